@@ -30,7 +30,7 @@ pseudorandom number generators", OOPSLA 2014): for ``i`` from ``P-1`` down to
 1, swap slot ``i`` with slot ``next() mod (i+1)``, the state starting at the
 seed.
 
-This oracle rescans a bitmap on every call (O(P)); it is slow on purpose.
+This oracle rescans the free flags on every call (O(P)); it is slow on purpose.
 
 Parity: the policy itself is underspecified in the paper, so agreement with
 the paper's allocator is "parity unpinned".  The reading above is pinned in
@@ -44,6 +44,8 @@ from __future__ import annotations
 
 from collections import deque
 from typing import List, Sequence
+
+import numpy as np
 
 POLICY_SEGMENT = 0
 POLICY_FIFO_SORTED = 1
@@ -85,20 +87,21 @@ def shuffled_ids(num_blocks: int, seed: int) -> List[int]:
     return a
 
 
-def free_runs_of(used: Sequence[int]) -> List[tuple]:
-    """Maximal runs ``(start, length)`` of zero entries, ascending by start."""
-    runs = []
-    i, P = 0, len(used)
-    while i < P:
-        if used[i]:
-            i += 1
-            continue
-        j = i
-        while j < P and not used[j]:
-            j += 1
-        runs.append((i, j - i))
-        i = j
-    return runs
+def free_run_arrays(used):
+    """Starts and lengths of the maximal runs of zero entries, ascending by
+    start.  A run starts where the used-flag falls from 1 to 0 (or at the
+    start) and ends where it rises again (or at the end)."""
+    u = np.asarray(used, dtype=np.int8)
+    edges = np.diff(np.concatenate(([1], u, [1])))
+    starts = np.flatnonzero(edges == -1)
+    ends = np.flatnonzero(edges == 1)
+    return starts, ends - starts
+
+
+def free_runs_of(used) -> List[tuple]:
+    """Maximal free runs as ``(start, length)`` tuples, ascending by start."""
+    starts, lens = free_run_arrays(used)
+    return [(int(a), int(b)) for a, b in zip(starts, lens)]
 
 
 class RefAllocator:
@@ -109,7 +112,7 @@ class RefAllocator:
             raise AllocError("inval", f"unknown policy {policy}")
         self.num_blocks = num_blocks
         self.policy = policy
-        self.used = bytearray(num_blocks)
+        self.used = np.zeros(num_blocks, dtype=np.uint8)
         if policy == POLICY_FIFO_SORTED:
             self.fifo = deque(range(num_blocks))
         elif policy == POLICY_FIFO_SHUFFLED:
@@ -119,7 +122,7 @@ class RefAllocator:
 
     # -- queries -----------------------------------------------------------
     def free_count(self) -> int:
-        return self.num_blocks - sum(self.used)
+        return self.num_blocks - int(self.used.sum())
 
     def stats(self):
         runs = free_runs_of(self.used)
@@ -139,47 +142,46 @@ class RefAllocator:
             out = [self.fifo.popleft() for _ in range(n)]
         else:
             out = []
-            runs = free_runs_of(self.used)
+            starts, lens = free_run_arrays(self.used)
             need = n
             while need > 0:
-                fitting = [r for r in runs if r[1] >= need]
-                if fitting:
-                    start, _ = min(fitting, key=lambda r: (r[1], r[0]))
-                    out.extend(range(start, start + need))
+                fitting = np.flatnonzero(lens >= need)
+                if fitting.size:
+                    # shortest fitting run; argmin keeps the first (lowest
+                    # start) of equally short runs
+                    k = fitting[np.argmin(lens[fitting])]
+                    out.extend(range(int(starts[k]), int(starts[k]) + need))
                     need = 0
                 else:
-                    big = max(runs, key=lambda r: (r[1], -r[0]))
-                    runs.remove(big)
-                    out.extend(range(big[0], big[0] + big[1]))
-                    need -= big[1]
-        for b in out:
-            self.used[b] = 1
+                    # longest run, taken whole; argmax keeps the lowest start
+                    k = int(np.argmax(lens))
+                    out.extend(range(int(starts[k]), int(starts[k] + lens[k])))
+                    need -= int(lens[k])
+                    starts, lens = np.delete(starts, k), np.delete(lens, k)
+        self.used[np.asarray(out, dtype=np.int64)] = 1
         return out
 
-    def _validate(self, ids: Sequence[int], want_used: bool):
-        seen = set()
-        for b in ids:
-            b = int(b)
-            if b < 0 or b >= self.num_blocks:
-                raise AllocError("range", f"block {b} outside [0, {self.num_blocks})")
-            if b in seen:
-                raise AllocError("dup", f"block {b} listed twice")
-            seen.add(b)
-        for b in ids:
-            if bool(self.used[int(b)]) != want_used:
-                raise AllocError("dup", f"block {int(b)} is {'free' if want_used else 'in use'}")
+    def _validate(self, ids: Sequence[int], want_used: bool) -> np.ndarray:
+        a = np.asarray(ids, dtype=np.int64).reshape(-1)
+        bad = a[(a < 0) | (a >= self.num_blocks)]
+        if bad.size:
+            raise AllocError("range", f"block {int(bad[0])} outside [0, {self.num_blocks})")
+        if np.unique(a).size != a.size:
+            raise AllocError("dup", "a block is listed twice")
+        wrong = a[self.used[a].astype(bool) != want_used]
+        if wrong.size:
+            raise AllocError("dup", f"block {int(wrong[0])} is {'free' if want_used else 'in use'}")
+        return a
 
     def free(self, ids: Sequence[int]) -> None:
-        self._validate(ids, want_used=True)
-        for b in ids:
-            self.used[int(b)] = 0
+        a = self._validate(ids, want_used=True)
+        self.used[a] = 0
         if self.fifo is not None:
-            self.fifo.extend(int(b) for b in ids)
+            self.fifo.extend(int(b) for b in a)
 
     def mark_used(self, ids: Sequence[int]) -> None:
-        self._validate(ids, want_used=False)
-        for b in ids:
-            self.used[int(b)] = 1
+        a = self._validate(ids, want_used=False)
+        self.used[a] = 1
         if self.fifo is not None:
-            gone = set(int(b) for b in ids)
+            gone = set(int(b) for b in a)
             self.fifo = deque(b for b in self.fifo if b not in gone)

@@ -105,7 +105,7 @@ def test_free_merges_neighbours():
 def test_errors_leave_state_unchanged():
     a = RefAllocator(6, POLICY_SEGMENT)
     got = a.alloc(4)
-    before = (bytes(a.used), a.stats())
+    before = (a.used.tobytes(), a.stats())
     with pytest.raises(NoSpace):
         a.alloc(3)
     for bad, kind in (([9], "range"), ([-1], "range"), ([0, 0], "dup"), ([4], "dup")):
@@ -116,7 +116,7 @@ def test_errors_leave_state_unchanged():
         a.mark_used([got[0]])
     with pytest.raises(AllocError):
         a.alloc(-1)
-    assert (bytes(a.used), a.stats()) == before
+    assert (a.used.tobytes(), a.stats()) == before
     assert a.alloc(0) == []
 
 
