@@ -1,0 +1,229 @@
+/*
+ * flowkv.h -- C ABI of the MI355X (gfx950) KV-cache transfer library.
+ *
+ * FlowKV (arXiv 2504.03775), section 3.3: after prefill, a request's KV cache
+ * (K and V of every layer, in fixed-size paged blocks) moves from the prefill
+ * side's block pool to the decode side's block pool.  Three pieces cut the
+ * number of transfer operations that scattered blocks cause:
+ *
+ *   flowkv_alloc*  -- a segment-based allocator that places a request in as few
+ *                     contiguous runs of block IDs as it can (section 3.3,
+ *                     allocator paragraph);
+ *   flowkv_plan*   -- bidirectional segment alignment: the runs of the request
+ *                     whose block IDs step by one on the sending and the
+ *                     receiving side together (section 3.3; Figure 3 caption);
+ *   flowkv_transfer -- one device launch that copies every run of every layer's
+ *                     K and V, in the per-layer layout (L, 2, B, H) or the
+ *                     block-major layout (B, L, 2, H) of Eq. 5, on one GPU.
+ *
+ * Conventions for every entry point:
+ *   - Functions return FLOWKV_OK (0) or a negative FLOWKV_E* code; nothing
+ *     throws across the ABI.  flowkv_strerror() names a code;
+ *     flowkv_last_error() gives the calling thread's last detailed message.
+ *   - On error, output arguments are left untouched, except *n_out of the
+ *     planners on FLOWKV_ECAP.
+ *   - The caller owns every buffer.  The library allocates no device memory and
+ *     keeps no pointer after a call returns, except inside an allocator handle.
+ *   - Block IDs and counts are int32; byte sizes and offsets are 64-bit.
+ *   - Allocator handles are not thread-safe; planners and the transfer are
+ *     reentrant.
+ */
+#ifndef FLOWKV_H
+#define FLOWKV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------------- */
+enum {
+  FLOWKV_OK = 0,
+  FLOWKV_EINVAL = -1, /* bad argument: NULL pointer, negative count, bad layout,
+                         misaligned or overlapping pools, unknown policy      */
+  FLOWKV_ENOSPC = -2, /* fewer free blocks than asked; allocator unchanged    */
+  FLOWKV_ERANGE = -3, /* a block ID outside [0, pool blocks)                  */
+  FLOWKV_EDUP = -4,   /* a block ID repeated where it must be unique, freeing
+                         a free block, or marking a used block               */
+  FLOWKV_ECAP = -5,   /* output capacity too small; *n_out holds the need     */
+  FLOWKV_EHIP = -6    /* the HIP runtime refused the launch                   */
+};
+
+/* ---- allocator policies ---------------------------------------------------- */
+enum {
+  /* Section 3.3 allocator: free blocks kept as maximal free runs; a request
+     takes the best-fitting run (shortest run that holds it, lowest start on
+     ties, blocks from its head); if no run holds it, it takes the longest runs
+     whole (lowest start on ties) until the rest fits one run, which is then
+     best-fitted -- the fewest runs any placement can use.  Freed blocks merge
+     with free neighbours. */
+  FLOWKV_POLICY_SEGMENT = 0,
+  /* Naive free list the paper contrasts with: FIFO of free IDs, ascending at
+     creation; alloc pops from the front, free appends in table order. */
+  FLOWKV_POLICY_FIFO_SORTED = 1,
+  /* Same FIFO, but starting as a seeded Fisher-Yates shuffle drawn from
+     SplitMix64 (Steele, Lea, Flood 2014): for i = P-1 down to 1, swap slot i
+     with slot next() mod (i+1), the generator state starting at the seed. */
+  FLOWKV_POLICY_FIFO_SHUFFLED = 2
+};
+
+/* ---- pool layouts (Eq. 5) -------------------------------------------------- */
+enum {
+  /* (L, 2, B, H): one device tensor per layer, each (2, B, H) -- K blocks then
+     V blocks.  layer_base[l] points at layer l's tensor. */
+  FLOWKV_LAYOUT_LAYER_MAJOR = 0,
+  /* (B, L, 2, H): one device tensor; a block's K and V of every layer are
+     adjacent.  layer_base[0] points at it. */
+  FLOWKV_LAYOUT_BLOCK_MAJOR = 1
+};
+
+#define FLOWKV_MAX_LAYERS 128
+
+typedef struct flowkv_allocator flowkv_allocator; /* opaque, host memory only */
+
+/* One aligned run: n_blocks blocks starting at src_block on the sender and at
+   dst_block on the receiver, all stepping by one together.  `first` is the
+   run's position in the plan's block order: the sum of n_blocks over all
+   earlier records of the same plan (a request's or a batch's), so a plan's
+   records tile [0, total blocks) in order.  16 bytes, 16-byte aligned. */
+typedef struct flowkv_segment {
+  int32_t src_block;
+  int32_t dst_block;
+  int32_t n_blocks;
+  int32_t first;
+} flowkv_segment;
+
+typedef struct flowkv_alloc_stats {
+  int64_t free_blocks;   /* blocks not in use                         */
+  int64_t free_segments; /* maximal runs of free block IDs            */
+  int64_t largest_free;  /* blocks in the longest free run            */
+} flowkv_alloc_stats;
+
+/* A paged KV pool on the device.  chunk_bytes is H times the element size:
+   the bytes of one (block, layer, K-or-V) slab, block_size tokens of
+   kv_heads x head_dim elements each.  A block holds 2 * num_layers chunks. */
+typedef struct flowkv_pool {
+  int32_t layout;          /* FLOWKV_LAYOUT_*                                 */
+  int32_t num_layers;      /* L, 1 .. FLOWKV_MAX_LAYERS                       */
+  int32_t num_blocks;      /* B, >= 1                                         */
+  int32_t reserved;        /* must be 0                                       */
+  int64_t chunk_bytes;     /* > 0, a multiple of 16                           */
+  void* const* layer_base; /* host array of device pointers, 16-byte aligned:
+                              num_layers entries (layer-major) or 1 entry
+                              (block-major)                                  */
+} flowkv_pool;
+
+/* Optional launch shape for flowkv_transfer_ex; a zero field takes the
+   library's choice.
+   threads: workgroup size, a multiple of 64 in 64..1024.
+   unroll:  16-byte vectors each thread moves per tile: 2, 4, 8 or 16.
+   grid:    workgroups to launch, >= 1 (capped at the number of tiles).
+   cache:   1 = plain loads and stores, 2 = nontemporal loads,
+            3 = nontemporal stores, 4 = nontemporal loads and stores. */
+typedef struct flowkv_launch_config {
+  int32_t threads;
+  int32_t unroll;
+  int32_t grid;
+  int32_t cache;
+} flowkv_launch_config;
+
+/* ---- allocator (section 3.3, allocator paragraph) -------------------------- */
+
+/* Create an allocator over block IDs [0, num_blocks), all free.  `seed` is used
+   by FLOWKV_POLICY_FIFO_SHUFFLED only.  *out receives the handle.
+   EINVAL: num_blocks < 0, unknown policy, out == NULL. */
+int flowkv_allocator_create(int32_t num_blocks, int32_t policy, uint64_t seed,
+                            flowkv_allocator** out);
+
+/* Release the handle (NULL is accepted). */
+void flowkv_allocator_destroy(flowkv_allocator* a);
+
+/* Allocate n_blocks blocks; out_ids[0 .. n_blocks) receives them in the
+   request's logical order.  All or nothing: ENOSPC when fewer are free, with
+   the allocator unchanged.  n_blocks == 0 succeeds and writes nothing.
+   EINVAL: a or out_ids NULL (out_ids may be NULL when n_blocks == 0),
+   n_blocks < 0. */
+int flowkv_alloc(flowkv_allocator* a, int32_t n_blocks, int32_t* out_ids);
+
+/* Return ids[0 .. n) to the free pool, merging with free neighbours.
+   ERANGE: an ID out of range; EDUP: an ID repeated or already free.  Checked
+   before any change: on error nothing is freed. */
+int flowkv_free(flowkv_allocator* a, const int32_t* ids, int32_t n);
+
+/* Mark ids[0 .. n) in use without allocating them (blocks already held by
+   resident requests).  ERANGE / EDUP as for flowkv_free, EDUP also for a block
+   already in use.  On error nothing changes. */
+int flowkv_mark_used(flowkv_allocator* a, const int32_t* ids, int32_t n);
+
+/* Current free-space summary. */
+int flowkv_allocator_stats(const flowkv_allocator* a, flowkv_alloc_stats* out);
+
+/* ---- bidirectional segment alignment (section 3.3; Figure 3 caption) ------- */
+
+/* Align one request: src_ids and dst_ids (n_blocks each, host memory) are the
+   sender's and the receiver's block lists in logical order.  Writes the
+   maximal runs with src and dst both stepping by +1 to out[0 .. *n_out), in
+   logical order, `first` counting from 0.
+   ERANGE: an ID outside its pool; EDUP: an ID repeated within src_ids or
+   within dst_ids; ECAP: more than `cap` runs (*n_out = runs needed);
+   EINVAL: NULL pointers (arrays may be NULL when n_blocks == 0), negative
+   sizes.  The run count is at most n_blocks. */
+int flowkv_plan(const int32_t* src_ids, const int32_t* dst_ids, int32_t n_blocks,
+                int32_t src_pool_blocks, int32_t dst_pool_blocks,
+                flowkv_segment* out, int64_t cap, int64_t* n_out);
+
+/* Align a batch of n_req requests in one call.  Request r's lists are
+   src_ids[offsets[r] .. offsets[r+1]) and the same range of dst_ids; offsets
+   has n_req + 1 non-decreasing entries starting at 0, and offsets[n_req] must
+   fit int32.  Runs never cross requests; `first` runs across the whole batch.
+   Receiver IDs must be distinct across the whole batch (one writer per
+   block); sender IDs must be distinct within a request but may repeat across
+   requests (shared prefix blocks).  Errors as for flowkv_plan. */
+int flowkv_plan_batch(int32_t n_req, const int64_t* offsets,
+                      const int32_t* src_ids, const int32_t* dst_ids,
+                      int32_t src_pool_blocks, int32_t dst_pool_blocks,
+                      flowkv_segment* out, int64_t cap, int64_t* n_out);
+
+/* ---- transfer (section 3.3, Eq. 5 layouts; one launch for the whole plan) --- */
+
+/* Enqueue one kernel on `hip_stream` (a hipStream_t; NULL = default stream)
+   that copies, for every run in segs_dev[0 .. n_segs) and every layer and K/V,
+   the run's blocks from `src` to `dst`.  segs_dev is device memory holding a
+   plan made by flowkv_plan/flowkv_plan_batch for pools of these sizes;
+   total_blocks is the plan's block count (last record's first + n_blocks).
+   The caller keeps segs_dev and both pools alive until the stream passes the
+   kernel.  Asynchronous: returns once the launch is enqueued.  n_segs == 0 or
+   total_blocks == 0 is a no-op.
+   The kernel checks every run against both pools and skips, never touches
+   outside the pools for, runs that fail the check.
+   EINVAL: NULL pointers, pools that disagree on num_layers or chunk_bytes,
+   bad layout, num_layers outside 1..FLOWKV_MAX_LAYERS, chunk_bytes not a
+   positive multiple of 16, a base pointer not 16-byte aligned, a block of
+   2 GiB or more, or src and dst memory ranges that overlap.
+   EHIP: the runtime rejected the launch (message in flowkv_last_error()). */
+int flowkv_transfer(const flowkv_pool* src, const flowkv_pool* dst,
+                    const flowkv_segment* segs_dev, int64_t n_segs,
+                    int64_t total_blocks, void* hip_stream);
+
+/* flowkv_transfer with an explicit launch shape (cfg may be NULL = default).
+   Same result for every valid shape; EINVAL for a shape outside the limits
+   documented at flowkv_launch_config. */
+int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst,
+                       const flowkv_segment* segs_dev, int64_t n_segs,
+                       int64_t total_blocks, const flowkv_launch_config* cfg,
+                       void* hip_stream);
+
+/* ---- diagnostics ------------------------------------------------------------ */
+
+/* Static name of a status code. */
+const char* flowkv_strerror(int code);
+
+/* The calling thread's most recent error message ("" if none). */
+const char* flowkv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLOWKV_H */

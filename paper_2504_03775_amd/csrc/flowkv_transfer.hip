@@ -1,0 +1,461 @@
+// Segment-coalesced KV-cache copy for gfx950 (MI355X).
+//
+// FlowKV (arXiv 2504.03775), section 3.3: after bidirectional segment
+// alignment every aligned run of blocks is moved by one operation, and Eq. 5's
+// block-major layout (B, L, 2, H) makes a block's K and V of every layer one
+// contiguous range.  Here the whole plan -- every run, every layer, K and V --
+// is one kernel launch on one device; the unit of work is a tile of
+// `unroll` lines, a line being one 16-byte vector per thread of a workgroup.
+//
+// Work decomposition.  A plan covers total_blocks logical blocks; block g's
+// bytes are split into tiles_per_block tiles, giving
+// units = total_blocks * tiles_per_block tiles.  Each workgroup takes a
+// contiguous range of units, finds the run holding its first block by binary
+// search over the runs' `first` fields, and then walks forward, so the run
+// lookup costs O(log runs) per workgroup plus one step per run crossed.
+//
+// Addressing.  Within a block, byte offset o belongs to chunk r = o / H
+// (layer r / 2, K for even r, V for odd r) at offset o % H.  Block-major
+// pools address base + b * BB + o; layer-major pools address
+// layer_base[l] + (kv * B + b) * H + o % H.  When H is a multiple of the line
+// (the usual case, H = 4 KiB or 32 KiB for Llama shapes), every line lies in
+// one chunk and all address arithmetic is wave-uniform: each load is a scalar
+// base plus the lane's 16-byte offset.  Other H use per-lane division by H
+// (Granlund-Montgomery multiply-shift) and the layer tables staged in LDS.
+//
+// The data is never interpreted: the copy is byte-exact for any dtype.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cstdint>
+
+#include "flowkv.h"
+#include "flowkv_status.h"
+
+using flowkv::fail;
+using flowkv::ok;
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+struct PoolArg {
+  char* base[FLOWKV_MAX_LAYERS];
+  int64_t num_blocks;
+};
+
+struct XferArgs {
+  PoolArg src;
+  PoolArg dst;
+  const flowkv_segment* segs;
+  int64_t chunk_bytes;      // H (bytes of one block/layer/K-or-V slab)
+  int64_t block_bytes;      // BB = 2 * L * H
+  int64_t units;            // total_blocks * tiles_per_block
+  int64_t units_per_wg;     // contiguous tiles per workgroup
+  int32_t n_segs;
+  int32_t num_layers;
+  int32_t lines_per_chunk;  // H / line bytes (uniform path only)
+  int32_t lines_per_block;  // ceil(BB / line bytes)
+  int32_t tiles_per_block;  // ceil(lines_per_block / unroll)
+  uint32_t h_magic;         // division by H (per-lane path)
+  uint32_t h_shift;
+  int32_t pad;
+};
+
+// Pool memory is global memory; naming the address space lets the compiler
+// emit global (not flat) vector loads and stores with a scalar base.
+typedef __attribute__((address_space(1))) u32x4 gvec;
+
+__device__ __forceinline__ const gvec* as_global(const char* p) {
+  return (const gvec*)(p);
+}
+__device__ __forceinline__ gvec* as_global(char* p) { return (gvec*)(p); }
+
+typedef __attribute__((address_space(4))) const flowkv_segment cseg;
+
+__device__ __forceinline__ flowkv_segment load_seg(const cseg* p) {
+  flowkv_segment s;
+  s.src_block = p->src_block;
+  s.dst_block = p->dst_block;
+  s.n_blocks = p->n_blocks;
+  s.first = p->first;
+  return s;
+}
+
+// kCache bit 0: nontemporal loads; bit 1: nontemporal stores.
+template <int kCache>
+__device__ __forceinline__ u32x4 load16(const gvec* p) {
+  if constexpr (kCache & 1) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+
+template <int kCache>
+__device__ __forceinline__ void store16(gvec* p, u32x4 v) {
+  if constexpr (kCache & 2) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+
+// Start of line j (0 <= j < lines_per_block) of block b when every line lies
+// in one chunk: chunk r = j / lines_per_chunk, line w = j % lines_per_chunk.
+template <bool kLM>
+__device__ __forceinline__ char* line_base(const PoolArg& p, const XferArgs& a, int64_t b,
+                                           int32_t j, int32_t r, int32_t w, int64_t line) {
+  if constexpr (kLM)
+    return p.base[r >> 1] + (int64_t(r & 1) * p.num_blocks + b) * a.chunk_bytes + int64_t(w) * line;
+  else
+    return p.base[0] + b * a.block_bytes + int64_t(j) * line;
+}
+
+// Tile t of a block when every line lies inside one chunk: all pointer
+// arithmetic is uniform across the workgroup; each lane adds its 16 bytes.
+template <bool kSrcLM, bool kDstLM, int kU, int kCache>
+__device__ __forceinline__ void copy_tile_uniform(const XferArgs& a, int64_t sb, int64_t db,
+                                                  int32_t t, int tid, int64_t line) {
+  const int32_t j0 = t * kU;
+  int32_t r = j0 / a.lines_per_chunk;
+  int32_t w = j0 - r * a.lines_per_chunk;
+  if (j0 + kU <= a.lines_per_block) {
+    // full tile: kU loads in flight, then kU stores, no branches between
+    // chunk and in-chunk line of every line of the tile (branch-free), then
+    // every layer base the tile needs, so those loads issue back to back
+    int32_t rr[kU], ww[kU];
+#pragma unroll
+    for (int i = 0; i < kU; ++i) {
+      rr[i] = r;
+      ww[i] = w;
+      const bool wrap = ++w == a.lines_per_chunk;
+      r += wrap;
+      w = wrap ? 0 : w;
+    }
+    char* sbase[kU];
+    char* dbase[kU];
+#pragma unroll
+    for (int i = 0; i < kU; ++i) {
+      sbase[i] = kSrcLM ? a.src.base[rr[i] >> 1] : a.src.base[0];
+      dbase[i] = kDstLM ? a.dst.base[rr[i] >> 1] : a.dst.base[0];
+    }
+    const gvec* sp[kU];
+    gvec* dp[kU];
+#pragma unroll
+    for (int i = 0; i < kU; ++i) {
+      const int64_t j = j0 + i;
+      sp[i] = as_global(kSrcLM ? sbase[i] + (int64_t(rr[i] & 1) * a.src.num_blocks + sb) * a.chunk_bytes + int64_t(ww[i]) * line
+                               : sbase[i] + sb * a.block_bytes + j * line) + tid;
+      dp[i] = as_global(kDstLM ? dbase[i] + (int64_t(rr[i] & 1) * a.dst.num_blocks + db) * a.chunk_bytes + int64_t(ww[i]) * line
+                               : dbase[i] + db * a.block_bytes + j * line) + tid;
+    }
+    u32x4 v[kU];
+#pragma unroll
+    for (int i = 0; i < kU; ++i) v[i] = load16<kCache>(sp[i]);
+#pragma unroll
+    for (int i = 0; i < kU; ++i) store16<kCache>(dp[i], v[i]);
+  } else {
+    // the block's last, short tile
+    for (int32_t j = j0; j < a.lines_per_block; ++j) {
+      const u32x4 v = load16<kCache>(as_global(line_base<kSrcLM>(a.src, a, sb, j, r, w, line)) + tid);
+      store16<kCache>(as_global(line_base<kDstLM>(a.dst, a, db, j, r, w, line)) + tid, v);
+      if (++w == a.lines_per_chunk) {
+        w = 0;
+        ++r;
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ uint32_t div_by_h(uint32_t o, uint32_t magic, uint32_t shift) {
+  const uint64_t hi = __umulhi(o, magic);
+  return uint32_t((hi + o) >> shift);
+}
+
+// Byte o of block b for any H (a multiple of 16): chunk r = o / H.
+template <bool kLM>
+__device__ __forceinline__ char* byte_addr(const PoolArg& p, char* const* lds_base,
+                                           const XferArgs& a, int64_t b, int64_t o) {
+  if constexpr (kLM) {
+    const uint32_t r = div_by_h(uint32_t(o), a.h_magic, a.h_shift);
+    const int64_t w = o - int64_t(r) * a.chunk_bytes;
+    return lds_base[r >> 1] + (int64_t(r & 1) * p.num_blocks + b) * a.chunk_bytes + w;
+  } else {
+    return p.base[0] + b * a.block_bytes + o;
+  }
+}
+
+// Tile t of a block for any H: each lane finds its own chunk.
+template <bool kSrcLM, bool kDstLM, int kU, int kCache>
+__device__ __forceinline__ void copy_tile_lanes(const XferArgs& a, char* const* s_src,
+                                                char* const* s_dst, int64_t sb, int64_t db,
+                                                int32_t t, int tid, int64_t line) {
+  const int64_t o0 = int64_t(t) * kU * line + int64_t(tid) * 16;
+  if (int64_t(t + 1) * kU * line <= a.block_bytes) {
+    const gvec* sp[kU];
+    gvec* dp[kU];
+#pragma unroll
+    for (int i = 0; i < kU; ++i) {
+      const int64_t o = o0 + int64_t(i) * line;
+      sp[i] = as_global(byte_addr<kSrcLM>(a.src, s_src, a, sb, o));
+      dp[i] = as_global(byte_addr<kDstLM>(a.dst, s_dst, a, db, o));
+    }
+    u32x4 v[kU];
+#pragma unroll
+    for (int i = 0; i < kU; ++i) v[i] = load16<kCache>(sp[i]);
+#pragma unroll
+    for (int i = 0; i < kU; ++i) store16<kCache>(dp[i], v[i]);
+  } else {
+    for (int64_t o = o0; o < a.block_bytes; o += line) {
+      const u32x4 v = load16<kCache>(as_global(byte_addr<kSrcLM>(a.src, s_src, a, sb, o)));
+      store16<kCache>(as_global(byte_addr<kDstLM>(a.dst, s_dst, a, db, o)), v);
+    }
+  }
+}
+
+template <bool kSrcLM, bool kDstLM, int kU, int kCache, bool kUniform>
+__global__ __launch_bounds__(1024) void kv_segment_copy(const XferArgs a) {
+  __shared__ char* s_src[kUniform ? 1 : FLOWKV_MAX_LAYERS];
+  __shared__ char* s_dst[kUniform ? 1 : FLOWKV_MAX_LAYERS];
+  const int tid = threadIdx.x;
+  const int64_t line = int64_t(blockDim.x) * 16;
+  int64_t u = int64_t(blockIdx.x) * a.units_per_wg;
+  const int64_t u_end = u + a.units_per_wg < a.units ? u + a.units_per_wg : a.units;
+  if (u >= u_end) return;  // uniform across the workgroup
+  if constexpr (!kUniform) {
+    for (int l = tid; l < a.num_layers; l += blockDim.x) {
+      s_src[l] = a.src.base[kSrcLM ? l : 0];
+      s_dst[l] = a.dst.base[kDstLM ? l : 0];
+    }
+    __syncthreads();
+  }
+
+  // The plan is read-only for the whole launch: reading it through the
+  // constant address space keeps the run lookups on the scalar unit.
+  const cseg* segs = (const cseg*)(a.segs);
+  int64_t g = u / a.tiles_per_block;
+  int32_t t = int32_t(u - g * a.tiles_per_block);
+  // the last run whose first block is <= g
+  int32_t lo = 0, hi = a.n_segs - 1;
+  while (lo < hi) {
+    const int32_t mid = (lo + hi + 1) >> 1;
+    if (segs[mid].first <= g) lo = mid;
+    else hi = mid - 1;
+  }
+  int32_t s = lo;
+  flowkv_segment seg = load_seg(segs + s);
+  for (; u < u_end; ++u) {
+    while (g - seg.first >= int64_t(seg.n_blocks) && s + 1 < a.n_segs) seg = load_seg(segs + ++s);
+    const int64_t off = g - seg.first;
+    const int64_t sb = int64_t(seg.src_block) + off;
+    const int64_t db = int64_t(seg.dst_block) + off;
+    // a record that does not cover g, or points outside a pool, moves nothing
+    const bool valid = off >= 0 && off < seg.n_blocks && sb >= 0 && sb < a.src.num_blocks &&
+                       db >= 0 && db < a.dst.num_blocks;
+    if (valid) {
+      if constexpr (kUniform)
+        copy_tile_uniform<kSrcLM, kDstLM, kU, kCache>(a, sb, db, t, tid, line);
+      else
+        copy_tile_lanes<kSrcLM, kDstLM, kU, kCache>(a, s_src, s_dst, sb, db, t, tid, line);
+    }
+    if (++t == a.tiles_per_block) {
+      t = 0;
+      ++g;
+    }
+  }
+}
+
+using KernelFn = void (*)(XferArgs);
+
+template <bool S, bool D, int U, int C>
+KernelFn pick_path(bool uniform) {
+  return uniform ? kv_segment_copy<S, D, U, C, true> : kv_segment_copy<S, D, U, C, false>;
+}
+
+template <bool S, bool D, int U>
+KernelFn pick_cache(int cache, bool uniform) {
+  switch (cache) {
+    case 0: return pick_path<S, D, U, 0>(uniform);
+    case 1: return pick_path<S, D, U, 1>(uniform);
+    case 2: return pick_path<S, D, U, 2>(uniform);
+    default: return pick_path<S, D, U, 3>(uniform);
+  }
+}
+
+template <bool S, bool D>
+KernelFn pick_unroll(int unroll, int cache, bool uniform) {
+  switch (unroll) {
+    case 2: return pick_cache<S, D, 2>(cache, uniform);
+    case 4: return pick_cache<S, D, 4>(cache, uniform);
+    case 8: return pick_cache<S, D, 8>(cache, uniform);
+    default: return pick_cache<S, D, 16>(cache, uniform);
+  }
+}
+
+KernelFn pick_kernel(bool src_lm, bool dst_lm, int unroll, int cache, bool uniform) {
+  if (src_lm && dst_lm) return pick_unroll<true, true>(unroll, cache, uniform);
+  if (src_lm) return pick_unroll<true, false>(unroll, cache, uniform);
+  if (dst_lm) return pick_unroll<false, true>(unroll, cache, uniform);
+  return pick_unroll<false, false>(unroll, cache, uniform);
+}
+
+// Library defaults (see the launch-shape sweep recorded with the profiles).
+constexpr int kDefaultThreads = 256;
+constexpr int kDefaultUnroll = 8;
+constexpr int kDefaultCache = 4;  // nontemporal loads and stores
+constexpr int kWavesPerCU = 32;
+
+std::atomic<int> g_cu_count[64];
+
+int cu_count(int* out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(FLOWKV_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev >= 0 && dev < 64) {
+    int c = g_cu_count[dev].load(std::memory_order_relaxed);
+    if (c > 0) {
+      *out = c;
+      return FLOWKV_OK;
+    }
+  }
+  int c = 0;
+  e = hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess || c <= 0)
+    return fail(FLOWKV_EHIP, "CU count query: %s", hipGetErrorString(e));
+  if (dev >= 0 && dev < 64) g_cu_count[dev].store(c, std::memory_order_relaxed);
+  *out = c;
+  return FLOWKV_OK;
+}
+
+struct Range {
+  uintptr_t lo, hi;
+};
+
+int pool_ranges(const flowkv_pool* p, const char* name, Range* out, int* n) {
+  if (!p) return fail(FLOWKV_EINVAL, "NULL %s pool", name);
+  if (p->layout != FLOWKV_LAYOUT_LAYER_MAJOR && p->layout != FLOWKV_LAYOUT_BLOCK_MAJOR)
+    return fail(FLOWKV_EINVAL, "%s pool: unknown layout %d", name, p->layout);
+  if (p->num_layers < 1 || p->num_layers > FLOWKV_MAX_LAYERS)
+    return fail(FLOWKV_EINVAL, "%s pool: %d layers, need 1..%d", name, p->num_layers,
+                FLOWKV_MAX_LAYERS);
+  if (p->num_blocks < 1) return fail(FLOWKV_EINVAL, "%s pool: %d blocks", name, p->num_blocks);
+  if (p->reserved != 0) return fail(FLOWKV_EINVAL, "%s pool: reserved field not 0", name);
+  if (p->chunk_bytes <= 0 || p->chunk_bytes % 16 != 0)
+    return fail(FLOWKV_EINVAL, "%s pool: chunk_bytes %lld not a positive multiple of 16", name,
+                (long long)p->chunk_bytes);
+  const int64_t block_bytes = 2 * int64_t(p->num_layers) * p->chunk_bytes;
+  if (block_bytes >= (int64_t(1) << 31))
+    return fail(FLOWKV_EINVAL, "%s pool: block of %lld bytes, limit 2 GiB", name,
+                (long long)block_bytes);
+  if (!p->layer_base) return fail(FLOWKV_EINVAL, "%s pool: NULL layer_base", name);
+  const bool lm = p->layout == FLOWKV_LAYOUT_LAYER_MAJOR;
+  const int nb = lm ? p->num_layers : 1;
+  const uint64_t bytes = lm ? uint64_t(2) * uint64_t(p->num_blocks) * uint64_t(p->chunk_bytes)
+                            : uint64_t(p->num_blocks) * uint64_t(block_bytes);
+  for (int i = 0; i < nb; ++i) {
+    uintptr_t b = reinterpret_cast<uintptr_t>(p->layer_base[i]);
+    if (!b) return fail(FLOWKV_EINVAL, "%s pool: NULL base pointer %d", name, i);
+    if (b % 16) return fail(FLOWKV_EINVAL, "%s pool: base pointer %d not 16-byte aligned", name, i);
+    out[i] = {b, b + uintptr_t(bytes)};
+  }
+  *n = nb;
+  return FLOWKV_OK;
+}
+
+bool overlaps(const Range& x, const Range& y) { return x.lo < y.hi && y.lo < x.hi; }
+
+}  // namespace
+
+extern "C" int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst,
+                                  const flowkv_segment* segs_dev, int64_t n_segs,
+                                  int64_t total_blocks, const flowkv_launch_config* cfg,
+                                  void* hip_stream) {
+  Range rs[FLOWKV_MAX_LAYERS], rd[FLOWKV_MAX_LAYERS];
+  int ns = 0, nd = 0;
+  int rc = pool_ranges(src, "sender", rs, &ns);
+  if (!rc) rc = pool_ranges(dst, "receiver", rd, &nd);
+  if (rc) return rc;
+  if (src->num_layers != dst->num_layers || src->chunk_bytes != dst->chunk_bytes)
+    return fail(FLOWKV_EINVAL, "pools disagree: %d vs %d layers, %lld vs %lld chunk bytes",
+                src->num_layers, dst->num_layers, (long long)src->chunk_bytes,
+                (long long)dst->chunk_bytes);
+  for (int i = 0; i < ns; ++i)
+    for (int j = 0; j < nd; ++j)
+      if (overlaps(rs[i], rd[j]))
+        return fail(FLOWKV_EINVAL, "sender tensor %d overlaps receiver tensor %d", i, j);
+  for (int i = 0; i < nd; ++i)
+    for (int j = i + 1; j < nd; ++j)
+      if (overlaps(rd[i], rd[j]))
+        return fail(FLOWKV_EINVAL, "receiver tensors %d and %d overlap", i, j);
+  if (n_segs < 0 || total_blocks < 0)
+    return fail(FLOWKV_EINVAL, "negative segment or block count");
+  if (n_segs > INT32_MAX || total_blocks > INT32_MAX)
+    return fail(FLOWKV_EINVAL, "segment or block count above 2^31-1");
+
+  int threads = kDefaultThreads, unroll = kDefaultUnroll, cache = kDefaultCache, grid = 0;
+  if (cfg) {
+    if (cfg->threads) threads = cfg->threads;
+    if (cfg->unroll) unroll = cfg->unroll;
+    if (cfg->cache) cache = cfg->cache;
+    grid = cfg->grid;
+  }
+  if (threads < 64 || threads > 1024 || threads % 64)
+    return fail(FLOWKV_EINVAL, "threads %d: need a multiple of 64 in 64..1024", threads);
+  if (unroll != 2 && unroll != 4 && unroll != 8 && unroll != 16)
+    return fail(FLOWKV_EINVAL, "unroll %d: need 2, 4, 8 or 16", unroll);
+  if (cache < 1 || cache > 4) return fail(FLOWKV_EINVAL, "cache %d: need 1..4", cache);
+  if (grid < 0) return fail(FLOWKV_EINVAL, "negative grid %d", grid);
+  if (n_segs == 0 || total_blocks == 0) return ok();
+  if (!segs_dev) return fail(FLOWKV_EINVAL, "NULL segment list");
+  if (reinterpret_cast<uintptr_t>(segs_dev) % 16)
+    return fail(FLOWKV_EINVAL, "segment list not 16-byte aligned");
+
+  XferArgs a{};
+  for (int i = 0; i < ns; ++i) a.src.base[i] = static_cast<char*>(src->layer_base[i]);
+  for (int i = 0; i < nd; ++i) a.dst.base[i] = static_cast<char*>(dst->layer_base[i]);
+  a.src.num_blocks = src->num_blocks;
+  a.dst.num_blocks = dst->num_blocks;
+  a.segs = segs_dev;
+  a.n_segs = int32_t(n_segs);
+  a.num_layers = src->num_layers;
+  a.chunk_bytes = src->chunk_bytes;
+  a.block_bytes = 2 * int64_t(src->num_layers) * src->chunk_bytes;
+  const int64_t line = int64_t(threads) * 16;
+  const bool uniform = a.chunk_bytes % line == 0;
+  a.lines_per_chunk = uniform ? int32_t(a.chunk_bytes / line) : 0;
+  a.lines_per_block = int32_t((a.block_bytes + line - 1) / line);
+  a.tiles_per_block = (a.lines_per_block + unroll - 1) / unroll;
+  // division by H for the per-lane path: l = ceil(log2 H),
+  // m = floor(2^32 (2^l - H) / H) + 1, q = (umulhi(o, m) + o) >> l
+  {
+    const uint64_t h = uint64_t(a.chunk_bytes);
+    uint32_t l = 0;
+    while ((uint64_t(1) << l) < h) ++l;
+    a.h_shift = l;
+    a.h_magic = uint32_t((((uint64_t(1) << l) - h) << 32) / h + 1);
+  }
+  a.units = total_blocks * int64_t(a.tiles_per_block);
+
+  if (grid == 0) {
+    int cus = 0;
+    rc = cu_count(&cus);
+    if (rc) return rc;
+    const int64_t per_cu = std::max<int64_t>(1, int64_t(kWavesPerCU) * 64 / threads);
+    grid = int(std::min<int64_t>(int64_t(cus) * per_cu, INT32_MAX));
+  }
+  const int64_t g = std::min<int64_t>(grid, a.units);
+  a.units_per_wg = (a.units + g - 1) / g;
+  const int64_t launch = (a.units + a.units_per_wg - 1) / a.units_per_wg;
+
+  KernelFn fn = pick_kernel(src->layout == FLOWKV_LAYOUT_LAYER_MAJOR,
+                            dst->layout == FLOWKV_LAYOUT_LAYER_MAJOR, unroll, cache - 1, uniform);
+  void* args[] = {&a};
+  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(launch)),
+                                 dim3(unsigned(threads)), args, 0,
+                                 static_cast<hipStream_t>(hip_stream));
+  if (e == hipSuccess) e = hipGetLastError();
+  if (e != hipSuccess) return fail(FLOWKV_EHIP, "kernel launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+extern "C" int flowkv_transfer(const flowkv_pool* src, const flowkv_pool* dst,
+                               const flowkv_segment* segs_dev, int64_t n_segs,
+                               int64_t total_blocks, void* hip_stream) {
+  return flowkv_transfer_ex(src, dst, segs_dev, n_segs, total_blocks, nullptr, hip_stream);
+}

@@ -1,0 +1,307 @@
+"""ctypes binding to ``libflowkv.so`` (the C ABI in ``include/flowkv.h``).
+
+Argument marshalling only: every step -- allocation, alignment, the copy --
+runs in the native library.  PyTorch supplies device memory and streams.
+The functions carry the C names; ``Allocator`` and ``KVPool`` are thin owners
+of a handle and of a pool descriptor.
+
+If the library is missing this module raises on import: there is no other
+code path.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libflowkv.so")
+
+OK, EINVAL, ENOSPC, ERANGE, EDUP, ECAP, EHIP = 0, -1, -2, -3, -4, -5, -6
+POLICY_SEGMENT, POLICY_FIFO_SORTED, POLICY_FIFO_SHUFFLED = 0, 1, 2
+LAYOUT_LAYER_MAJOR, LAYOUT_BLOCK_MAJOR = 0, 1
+MAX_LAYERS = 128
+
+SEGMENT_DTYPE = np.dtype([("src_block", "<i4"), ("dst_block", "<i4"),
+                          ("n_blocks", "<i4"), ("first", "<i4")])
+
+
+class FlowKVError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        msg = _lib.flowkv_last_error().decode() or _lib.flowkv_strerror(code).decode()
+        super().__init__(f"{where}: {_lib.flowkv_strerror(code).decode()} ({code}): {msg}")
+
+
+class flowkv_segment(ctypes.Structure):
+    _fields_ = [("src_block", ctypes.c_int32), ("dst_block", ctypes.c_int32),
+                ("n_blocks", ctypes.c_int32), ("first", ctypes.c_int32)]
+
+
+class flowkv_alloc_stats(ctypes.Structure):
+    _fields_ = [("free_blocks", ctypes.c_int64), ("free_segments", ctypes.c_int64),
+                ("largest_free", ctypes.c_int64)]
+
+
+class flowkv_pool(ctypes.Structure):
+    _fields_ = [("layout", ctypes.c_int32), ("num_layers", ctypes.c_int32),
+                ("num_blocks", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("chunk_bytes", ctypes.c_int64), ("layer_base", ctypes.POINTER(ctypes.c_void_p))]
+
+
+class flowkv_launch_config(ctypes.Structure):
+    _fields_ = [("threads", ctypes.c_int32), ("unroll", ctypes.c_int32),
+                ("grid", ctypes.c_int32), ("cache", ctypes.c_int32)]
+
+
+_I32P = ctypes.POINTER(ctypes.c_int32)
+_I64P = ctypes.POINTER(ctypes.c_int64)
+_SEGP = ctypes.POINTER(flowkv_segment)
+_POOLP = ctypes.POINTER(flowkv_pool)
+
+# name -> (restype, argtypes); the exported symbol set of include/flowkv.h
+SIGNATURES = {
+    "flowkv_allocator_create": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_uint64,
+                                               ctypes.POINTER(ctypes.c_void_p)]),
+    "flowkv_allocator_destroy": (None, [ctypes.c_void_p]),
+    "flowkv_alloc": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, _I32P]),
+    "flowkv_free": (ctypes.c_int, [ctypes.c_void_p, _I32P, ctypes.c_int32]),
+    "flowkv_mark_used": (ctypes.c_int, [ctypes.c_void_p, _I32P, ctypes.c_int32]),
+    "flowkv_allocator_stats": (ctypes.c_int, [ctypes.c_void_p,
+                                              ctypes.POINTER(flowkv_alloc_stats)]),
+    "flowkv_plan": (ctypes.c_int, [_I32P, _I32P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                   _SEGP, ctypes.c_int64, _I64P]),
+    "flowkv_plan_batch": (ctypes.c_int, [ctypes.c_int32, _I64P, _I32P, _I32P, ctypes.c_int32,
+                                         ctypes.c_int32, _SEGP, ctypes.c_int64, _I64P]),
+    "flowkv_transfer": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_int64,
+                                       ctypes.c_int64, ctypes.c_void_p]),
+    "flowkv_transfer_ex": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_int64,
+                                          ctypes.c_int64, ctypes.POINTER(flowkv_launch_config),
+                                          ctypes.c_void_p]),
+    "flowkv_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+    "flowkv_last_error": (ctypes.c_char_p, []),
+}
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run paper_2504_03775_amd.build.build() "
+                          "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(LIB_PATH)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+def lib():
+    return _lib
+
+
+def _check(rc: int, where: str):
+    if rc != OK:
+        raise FlowKVError(rc, where)
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _ptr(a: np.ndarray, t=_I32P):
+    return a.ctypes.data_as(t)
+
+
+# ---- allocator ---------------------------------------------------------------
+
+def flowkv_allocator_create(num_blocks: int, policy: int = POLICY_SEGMENT, seed: int = 0):
+    h = ctypes.c_void_p()
+    _check(_lib.flowkv_allocator_create(num_blocks, policy, seed & (2**64 - 1), ctypes.byref(h)),
+           "flowkv_allocator_create")
+    return h
+
+
+def flowkv_allocator_destroy(h) -> None:
+    _lib.flowkv_allocator_destroy(h)
+
+
+def flowkv_alloc(h, n_blocks: int) -> np.ndarray:
+    out = np.empty(max(n_blocks, 0), dtype=np.int32)
+    _check(_lib.flowkv_alloc(h, n_blocks, _ptr(out)), "flowkv_alloc")
+    return out
+
+
+def flowkv_free(h, ids) -> None:
+    ids = _i32(ids)
+    _check(_lib.flowkv_free(h, _ptr(ids), ids.size), "flowkv_free")
+
+
+def flowkv_mark_used(h, ids) -> None:
+    ids = _i32(ids)
+    _check(_lib.flowkv_mark_used(h, _ptr(ids), ids.size), "flowkv_mark_used")
+
+
+def flowkv_allocator_stats(h) -> dict:
+    st = flowkv_alloc_stats()
+    _check(_lib.flowkv_allocator_stats(h, ctypes.byref(st)), "flowkv_allocator_stats")
+    return {"free_blocks": st.free_blocks, "free_segments": st.free_segments,
+            "largest_free": st.largest_free}
+
+
+class Allocator:
+    """Owner of one allocator handle."""
+
+    def __init__(self, num_blocks: int, policy: int = POLICY_SEGMENT, seed: int = 0):
+        self.num_blocks = num_blocks
+        self.policy = policy
+        self._h = flowkv_allocator_create(num_blocks, policy, seed)
+
+    def __del__(self):
+        h, self._h = getattr(self, "_h", None), None
+        if h:
+            flowkv_allocator_destroy(h)
+
+    def alloc(self, n: int) -> np.ndarray:
+        return flowkv_alloc(self._h, n)
+
+    def free(self, ids) -> None:
+        flowkv_free(self._h, ids)
+
+    def mark_used(self, ids) -> None:
+        flowkv_mark_used(self._h, ids)
+
+    def stats(self) -> dict:
+        return flowkv_allocator_stats(self._h)
+
+
+# ---- planner -----------------------------------------------------------------
+
+def flowkv_plan(src_ids, dst_ids, src_pool_blocks: int, dst_pool_blocks: int) -> np.ndarray:
+    """Aligned runs of one request as a SEGMENT_DTYPE array."""
+    s, d = _i32(src_ids), _i32(dst_ids)
+    if s.size != d.size:
+        raise ValueError("sender and receiver lists differ in length")
+    out = np.empty(max(s.size, 1), dtype=SEGMENT_DTYPE)
+    n = ctypes.c_int64()
+    _check(_lib.flowkv_plan(_ptr(s), _ptr(d), s.size, src_pool_blocks, dst_pool_blocks,
+                            out.ctypes.data_as(_SEGP), out.size, ctypes.byref(n)), "flowkv_plan")
+    return out[: n.value]
+
+
+def flowkv_plan_batch(offsets, src_ids, dst_ids, src_pool_blocks: int,
+                      dst_pool_blocks: int) -> np.ndarray:
+    """Aligned runs of a batch (request r = offsets[r] .. offsets[r+1])."""
+    off = np.ascontiguousarray(np.asarray(offsets, dtype=np.int64))
+    s, d = _i32(src_ids), _i32(dst_ids)
+    if s.size != d.size:
+        raise ValueError("sender and receiver lists differ in length")
+    out = np.empty(max(s.size, 1), dtype=SEGMENT_DTYPE)
+    n = ctypes.c_int64()
+    _check(_lib.flowkv_plan_batch(off.size - 1, _ptr(off, _I64P), _ptr(s), _ptr(d),
+                                  src_pool_blocks, dst_pool_blocks, out.ctypes.data_as(_SEGP),
+                                  out.size, ctypes.byref(n)), "flowkv_plan_batch")
+    return out[: n.value]
+
+
+def plan_total_blocks(segs: np.ndarray) -> int:
+    if segs.size == 0:
+        return 0
+    return int(segs["first"][-1]) + int(segs["n_blocks"][-1])
+
+
+# ---- pools and transfer ------------------------------------------------------
+
+class KVPool:
+    """Device pool descriptor over caller-owned torch tensors.
+
+    Block-major: one contiguous tensor shaped (B, L, 2, block_size, kv_heads,
+    head_dim).  Layer-major: a list of L contiguous tensors, each shaped
+    (2, B, block_size, kv_heads, head_dim).
+    """
+
+    def __init__(self, layout: int, tensors):
+        import torch  # device memory only
+
+        if layout == LAYOUT_BLOCK_MAJOR:
+            t = tensors[0] if isinstance(tensors, (list, tuple)) else tensors
+            if t.dim() != 6:
+                raise ValueError("block-major pool tensor must be (B, L, 2, bs, Hkv, Dh)")
+            B, L, two, bs, hkv, dh = t.shape
+            self.tensors = [t]
+        elif layout == LAYOUT_LAYER_MAJOR:
+            ts = list(tensors)
+            if not ts or any(x.dim() != 5 for x in ts):
+                raise ValueError("layer-major pool needs L tensors shaped (2, B, bs, Hkv, Dh)")
+            two, B, bs, hkv, dh = ts[0].shape
+            L = len(ts)
+            if any(tuple(x.shape) != tuple(ts[0].shape) or x.dtype != ts[0].dtype for x in ts):
+                raise ValueError("layer tensors differ in shape or dtype")
+            self.tensors = ts
+        else:
+            raise ValueError(f"unknown layout {layout}")
+        if two != 2:
+            raise ValueError("the K/V axis must have size 2")
+        for x in self.tensors:
+            if not x.is_contiguous() or x.device.type != "cuda":
+                raise ValueError("pool tensors must be contiguous device tensors")
+        self.layout, self.num_layers, self.num_blocks = layout, L, B
+        self.block_size, self.kv_heads, self.head_dim = bs, hkv, dh
+        self.elem_bytes = self.tensors[0].element_size()
+        self.chunk_bytes = bs * hkv * dh * self.elem_bytes
+        self.block_bytes = 2 * L * self.chunk_bytes
+        self.device = self.tensors[0].device
+        self._bases = (ctypes.c_void_p * len(self.tensors))(*[x.data_ptr() for x in self.tensors])
+        self.desc = flowkv_pool(layout, L, B, 0, self.chunk_bytes,
+                                ctypes.cast(self._bases, ctypes.POINTER(ctypes.c_void_p)))
+
+
+def _stream_handle(stream) -> Optional[int]:
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def flowkv_transfer(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_blocks: int,
+                    stream=None) -> None:
+    """Enqueue the one-launch copy; segs_dev is a device int32 (k, 4) tensor."""
+    _check(_lib.flowkv_transfer(ctypes.byref(src.desc), ctypes.byref(dst.desc),
+                                ctypes.c_void_p(segs_dev.data_ptr() if n_segs else 0), n_segs,
+                                total_blocks, ctypes.c_void_p(_stream_handle(stream))),
+           "flowkv_transfer")
+
+
+def flowkv_transfer_ex(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_blocks: int,
+                       threads: int = 0, unroll: int = 0, grid: int = 0, cache: int = 0,
+                       stream=None) -> None:
+    cfg = flowkv_launch_config(threads, unroll, grid, cache)
+    _check(_lib.flowkv_transfer_ex(ctypes.byref(src.desc), ctypes.byref(dst.desc),
+                                   ctypes.c_void_p(segs_dev.data_ptr() if n_segs else 0),
+                                   n_segs, total_blocks, ctypes.byref(cfg),
+                                   ctypes.c_void_p(_stream_handle(stream))),
+           "flowkv_transfer_ex")
+
+
+def segments_to_device(segs: np.ndarray, device, stream=None):
+    """Stage a plan in pinned memory and copy it to the device on `stream`.
+
+    Returns the device tensor (int32, (k, 4)); it must outlive the transfer
+    that reads it (torch's caching allocator keeps it while referenced)."""
+    import torch
+
+    host = torch.from_numpy(np.ascontiguousarray(segs).view(np.int32).reshape(-1, 4))
+    pinned = host.pin_memory()
+    if stream is None:
+        return pinned.to(device, non_blocking=True)
+    with torch.cuda.stream(stream):
+        return pinned.to(device, non_blocking=True)
+
+
+def strerror(code: int) -> str:
+    return _lib.flowkv_strerror(code).decode()

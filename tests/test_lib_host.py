@@ -1,0 +1,255 @@
+"""Host-side parity of the native library (CPU only, no kernel launches).
+
+The allocator and the planner of ``libflowkv.so`` run on the host; here they
+are checked against the oracle on the same seeded inputs: identical block
+lists from every allocator policy, identical runs from the planner, and every
+error path of the C ABI forced from the host.
+"""
+
+import ctypes
+import re
+import os
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+import oracle
+from paper_2504_03775_amd import flowkv as fk
+from workloads import churn_ops, replay, occupied_blocks, SEED_OCCUPANCY
+from workloads import recipes
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "flowkv.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(flowkv_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert len(names) >= 12
+    lib = ctypes.CDLL(fk.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(fk.SIGNATURES)
+
+
+def test_strerror_names_every_code():
+    for c in (fk.OK, fk.EINVAL, fk.ENOSPC, fk.ERANGE, fk.EDUP, fk.ECAP, fk.EHIP):
+        assert fk.strerror(c) and fk.strerror(c) != "unknown status code"
+    assert fk.strerror(12345) == "unknown status code"
+
+
+# ---- allocator ---------------------------------------------------------------
+
+def both(P, policy, seed=0):
+    return fk.Allocator(P, policy, seed), oracle.RefAllocator(P, policy, seed)
+
+
+@pytest.mark.parametrize("policy", [0, 1, 2])
+@settings(max_examples=80, deadline=None)
+@given(seed=st.integers(0, 2**63 - 1))
+def test_allocator_matches_oracle_on_random_streams(policy, seed):
+    g = np.random.default_rng(seed)
+    P = int(g.integers(1, 300))
+    a, r = both(P, policy, seed)
+    pre = g.permutation(P)[: int(g.integers(0, P // 2 + 1))]
+    a.mark_used(pre)
+    r.mark_used(pre)
+    live = []
+    for _ in range(80):
+        if live and g.random() < 0.45:
+            ids = live.pop(int(g.integers(len(live))))
+            a.free(ids)
+            r.free(ids)
+        else:
+            n = int(g.integers(0, P // 3 + 2))
+            if n > r.free_count():
+                with pytest.raises(fk.FlowKVError) as e:
+                    a.alloc(n)
+                assert e.value.code == fk.ENOSPC
+                with pytest.raises(oracle.NoSpace):
+                    r.alloc(n)
+                continue
+            x, y = a.alloc(n), r.alloc(n)
+            assert x.tolist() == list(y)
+            live.append(x)
+        assert a.stats() == r.stats()
+
+
+@pytest.mark.parametrize("variant", ["segment", "shuffled"])
+def test_churn_stream_full_size_identical_tables(variant):
+    """The 10,000-op churn workload at its real pool size (65,536 blocks)."""
+    wl_c = recipes.churn(lambda P, pol, s: fk.Allocator(P, pol, s), variant)
+    wl_o = recipes.churn(lambda P, pol, s: oracle.RefAllocator(P, pol, s), variant)
+    assert len(wl_c.tables) == len(wl_o.tables) == 128
+    for (s1, d1), (s2, d2) in zip(wl_c.tables, wl_o.tables):
+        assert np.array_equal(s1, s2) and np.array_equal(d1, d2)
+
+
+def test_llama8b_tables_identical_and_fragmented():
+    for pol in ("fifo_sorted", "segment"):
+        wc = recipes.llama8b_13k(lambda P, p, s: fk.Allocator(P, p, s), pol)
+        wo = recipes.llama8b_13k(lambda P, p, s: oracle.RefAllocator(P, p, s), pol)
+        (S1, D1), (S2, D2) = wc.tables[0], wo.tables[0]
+        assert np.array_equal(S1, S2) and np.array_equal(D1, D2)
+        assert S1.tolist() == list(range(813))
+        k = len(oracle.plan_ref(S1.tolist(), D1.tolist()))
+        assert (150 < k < 400) if pol == "fifo_sorted" else (10 < k < 100)
+
+
+def test_allocator_errors():
+    a = fk.Allocator(10)
+    ids = a.alloc(6)
+    before = a.stats()
+    cases = [(lambda: a.alloc(5), fk.ENOSPC), (lambda: a.alloc(-1), fk.EINVAL),
+             (lambda: a.free([10]), fk.ERANGE), (lambda: a.free([-1]), fk.ERANGE),
+             (lambda: a.free([ids[0], ids[0]]), fk.EDUP), (lambda: a.free([8]), fk.EDUP),
+             (lambda: a.mark_used([ids[1]]), fk.EDUP), (lambda: a.mark_used([7, 7]), fk.EDUP)]
+    for fn, code in cases:
+        with pytest.raises(fk.FlowKVError) as e:
+            fn()
+        assert e.value.code == code
+    assert a.stats() == before
+    assert a.alloc(0).size == 0
+    for bad in ((-1, 0), (5, 7)):
+        with pytest.raises(fk.FlowKVError) as e:
+            fk.Allocator(*bad)
+        assert e.value.code == fk.EINVAL
+
+
+# ---- planner -----------------------------------------------------------------
+
+def as_tuples(segs):
+    return [(int(s["src_block"]), int(s["dst_block"]), int(s["n_blocks"])) for s in segs]
+
+
+@settings(max_examples=300, deadline=None)
+@given(st.data())
+def test_plan_matches_oracle(data):
+    seed = data.draw(st.integers(0, 2**32 - 1))
+    g = np.random.default_rng(seed)
+    P = int(g.integers(1, 200))
+    n = int(g.integers(0, P + 1))
+    S = g.permutation(P)[:n]
+    D = g.permutation(P)[:n]
+    for i in range(1, n):  # contiguous stretches are the interesting case
+        if g.random() < 0.7 and S[i - 1] + 1 < P and D[i - 1] + 1 < P \
+                and S[i - 1] + 1 not in S[:i] and D[i - 1] + 1 not in D[:i]:
+            j = np.flatnonzero(S == S[i - 1] + 1)
+            k = np.flatnonzero(D == D[i - 1] + 1)
+            if j.size: S[j[0]] = S[i]
+            if k.size: D[k[0]] = D[i]
+            S[i], D[i] = S[i - 1] + 1, D[i - 1] + 1
+    if len(set(S.tolist())) < n or len(set(D.tolist())) < n:
+        return
+    segs = fk.flowkv_plan(S, D, P, P)
+    assert as_tuples(segs) == oracle.plan_ref(S.tolist(), D.tolist())
+    assert segs["first"].tolist() == np.concatenate(([0], np.cumsum(segs["n_blocks"])[:-1])).tolist()[:len(segs)]
+
+
+def test_plan_batch_matches_oracle_and_first_runs_across_batch():
+    g = np.random.default_rng(5)
+    tables = []
+    for n in (5, 0, 9, 1, 7):
+        tables.append((g.permutation(40)[:n], g.permutation(100)[:n]))
+    # receiver IDs must be disjoint across requests: shift each request
+    tables = [(s, d + 100 * i) for i, (s, d) in enumerate(tables)]
+    off = np.concatenate(([0], np.cumsum([len(s) for s, _ in tables])))
+    S = np.concatenate([s for s, _ in tables])
+    D = np.concatenate([d for _, d in tables])
+    segs = fk.flowkv_plan_batch(off, S, D, 40, 500)
+    ref = oracle.plan_batch_ref([(s.tolist(), d.tolist()) for s, d in tables])
+    assert as_tuples(segs) == [r[:3] for r in ref]
+    assert segs["first"][0] == 0
+    assert (segs["first"][1:] == np.cumsum(segs["n_blocks"])[:-1]).all()
+    assert fk.plan_total_blocks(segs) == len(S)
+
+
+def test_plan_contiguous_is_one_and_stride2_is_n():
+    n = 813
+    segs = fk.flowkv_plan(np.arange(n), np.arange(100, 100 + n), 1000, 1000)
+    assert as_tuples(segs) == [(0, 100, n)]
+    segs = fk.flowkv_plan(2 * np.arange(n), 2 * np.arange(n) + 1, 2000, 2000)
+    assert len(segs) == n
+
+
+def test_plan_errors():
+    P = 16
+    cases = [((P,), (0,), fk.ERANGE), ((0,), (-1,), fk.ERANGE), ((1, 1), (2, 3), fk.EDUP),
+             ((1, 2), (3, 3), fk.EDUP)]
+    for S, D, code in cases:
+        with pytest.raises(fk.FlowKVError) as e:
+            fk.flowkv_plan(S, D, P, P)
+        assert e.value.code == code
+    # ECAP reports the need
+    S = np.array([0, 2, 4], dtype=np.int32)
+    D = np.array([0, 1, 2], dtype=np.int32)
+    out = (fk.flowkv_segment * 1)()
+    need = ctypes.c_int64(-7)
+    rc = fk.lib().flowkv_plan(S.ctypes.data_as(fk._I32P), D.ctypes.data_as(fk._I32P), 3, P, P,
+                              out, 1, ctypes.byref(need))
+    assert rc == fk.ECAP and need.value == 3
+    # batch: a receiver block shared by two requests is rejected, a sender
+    # block shared by two requests is allowed
+    with pytest.raises(fk.FlowKVError) as e:
+        fk.flowkv_plan_batch([0, 1, 2], [1, 2], [5, 5], P, P)
+    assert e.value.code == fk.EDUP
+    assert len(fk.flowkv_plan_batch([0, 1, 2], [1, 1], [5, 6], P, P)) == 2
+    for off in ([1, 2], [0, 2, 1]):
+        with pytest.raises(fk.FlowKVError) as e:
+            fk.flowkv_plan_batch(off, [1, 2], [3, 4], P, P)
+        assert e.value.code == fk.EINVAL
+    assert len(fk.flowkv_plan([], [], P, P)) == 0
+
+
+# ---- transfer argument checks (rejected before any device call) --------------
+
+def pool(layout=1, L=2, B=8, chunk=4096, bases=(1 << 20,)):
+    arr = (ctypes.c_void_p * len(bases))(*bases)
+    p = fk.flowkv_pool(layout, L, B, 0, chunk, ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p)))
+    p._keep = arr
+    return p
+
+
+def xfer(src, dst, n_segs=1, total=1, cfg=None, segs=1 << 12):
+    c = ctypes.byref(cfg) if cfg is not None else None
+    return fk.lib().flowkv_transfer_ex(ctypes.byref(src), ctypes.byref(dst),
+                                       ctypes.c_void_p(segs), n_segs, total, c, None)
+
+
+def test_transfer_rejects_bad_pools_without_touching_the_device():
+    bb = 2 * 2 * 4096
+    good_src = pool(bases=(1 << 30,))
+    good_dst = pool(bases=(1 << 31,))
+    # no-op plans succeed without a launch
+    assert xfer(good_src, good_dst, n_segs=0, total=0) == fk.OK
+    assert xfer(good_src, good_dst, n_segs=5, total=0) == fk.OK
+    bad = [
+        (pool(bases=(1 << 30,)), pool(bases=((1 << 30) + bb,))),          # overlap
+        (pool(bases=((1 << 30) + 8,)), good_dst),                           # misaligned
+        (pool(chunk=100, bases=(1 << 30,)), pool(chunk=100, bases=(1 << 31,))),  # not x16
+        (pool(L=129, bases=(1 << 30,)), pool(L=129, bases=(1 << 31,))),     # too many layers
+        (pool(L=3, bases=(1 << 30,)), good_dst),                            # layer mismatch
+        (pool(layout=7, bases=(1 << 30,)), good_dst),                       # bad layout
+        (pool(B=0, bases=(1 << 30,)), good_dst),                            # empty pool
+        (pool(bases=(0,)), good_dst),                                       # NULL base
+        (pool(L=128, chunk=1 << 23, bases=(1 << 30,)), pool(L=128, chunk=1 << 23, bases=(1 << 40,))),
+        (pool(layout=0, L=2, bases=(1 << 30, 1 << 30)), good_dst),         # fine for src ...
+    ]
+    for i, (s, d) in enumerate(bad[:-1]):
+        assert xfer(s, d) == fk.EINVAL, i
+    # receiver layer tensors that overlap each other
+    d = pool(layout=0, L=2, bases=(1 << 33, (1 << 33) + 4096))
+    assert xfer(good_src, d, n_segs=0, total=0) == fk.EINVAL
+    # launch shapes outside the documented limits
+    for cfg in (fk.flowkv_launch_config(96, 8, 0, 0), fk.flowkv_launch_config(2048, 8, 0, 0),
+                fk.flowkv_launch_config(256, 3, 0, 0), fk.flowkv_launch_config(256, 8, -1, 0),
+                fk.flowkv_launch_config(256, 8, 0, 9)):
+        assert xfer(good_src, good_dst, n_segs=0, total=0, cfg=cfg) == fk.EINVAL
+    assert xfer(good_src, good_dst, segs=8) == fk.EINVAL  # misaligned plan
+    assert xfer(good_src, good_dst, segs=0) == fk.EINVAL  # NULL plan
+    assert xfer(good_src, good_dst, n_segs=-1) == fk.EINVAL
