@@ -1,0 +1,304 @@
+"""Benchmark: one Llama-3-8B-shape 13,000-token request's KV cache moved
+between two paged pools on one MI355X.
+
+A step is one pass of the whole hot path for one request:
+  1. the receiver's segment allocator places the request's 813 blocks in its
+     30%-occupied 65,536-block pool (host),
+  2. bidirectional segment alignment of the sender's and receiver's block
+     lists (host),
+  3. the plan is staged through pinned memory to the device (one small copy),
+  4. one kernel launch moves every run's K and V of all 32 layers,
+  5. the receiver's blocks are released again so every step sees the same
+     pool state (host bookkeeping, after the launch).
+Steps are enqueued back to back on one stream; host work overlaps the
+previous step's kernel.  Inputs are resident in HBM before timing starts.
+
+Prints one JSON line.  `value` is the effective transfer rate (payload bytes
+of K and V moved per second over the timed steps); `roofline` prices the
+transfer kernel's own launches (events around each launch on its stream)
+against the 8 TB/s HBM peak with 2x payload (read + write) of traffic;
+`cpu_baseline` is the oracle (numpy, one thread) moving the same request on
+the host.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "effective KV transfer GB/s (% of HBM peak); ms per 13k-token request transfer"
+KERNEL_SRC = os.path.join(ROOT, "paper_2504_03775_amd", "csrc", "flowkv_transfer.hip")
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "kv_segment_copy_llama3-8b-13k_pmc.txt")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--layout", choices=["block", "layer"], default="block",
+                    help="pool layout of both sides: Eq. 5 block-major or per-layer")
+    ap.add_argument("--dst-policy", choices=["segment", "fifo_sorted"], default="segment")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-context", action="store_true",
+                    help="skip the memcpy comparators and the flushed-cache timing")
+    ap.add_argument("--threads", type=int, default=0)
+    ap.add_argument("--unroll", type=int, default=0)
+    ap.add_argument("--grid", type=int, default=0)
+    ap.add_argument("--cache", type=int, default=0)
+    ap.add_argument("--calibrate-copy-gib", type=float, default=1.0,
+                    help="size of the plain copy run beside the kernel (HBM counter scale)")
+    return ap.parse_args()
+
+
+def kernel_hash() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def traffic_from_profile(per_launch_payload: int):
+    """HBM bytes per launch from the committed counter summary, scaled by the
+    plain-copy calibration recorded with it; None if absent or if the kernel
+    source changed since the counters were taken."""
+    if not os.path.exists(PMC_SUMMARY):
+        return None
+    text = open(PMC_SUMMARY).read()
+    m = re.search(r"kernel_source_sha256_16:\s*(\w+)", text)
+    if not m or m.group(1) != kernel_hash():
+        return None
+    t = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    return float(t.group(1)) if t else None
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the transfer "
+              "path in this build is single-device.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2504_03775_amd import flowkv as fk
+    from workloads import (LLAMA3_8B, SEED_DST_TABLE, SEED_OCCUPANCY, SEED_SRC_TABLE,
+                           blocks_for, make_device_pool, occupied_blocks)
+    from workloads.recipes import POLICIES
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    geom = LLAMA3_8B
+    tokens, pool_blocks = 13_000, 65_536
+    n = blocks_for(tokens, geom.block_size)
+    layout = fk.LAYOUT_BLOCK_MAJOR if args.layout == "block" else fk.LAYOUT_LAYER_MAJOR
+    payload = n * geom.block_bytes
+
+    # ---- setup (untimed): pools, sender's list, receiver's allocator ----------
+    free, total = torch.cuda.mem_get_info()
+    need = 2 * pool_blocks * geom.block_bytes
+    dst_blocks = pool_blocks
+    if need > free - (4 << 30):
+        dst_blocks = int(((free - (4 << 30)) // geom.block_bytes - pool_blocks) // 4096 * 4096)
+        print(f"note: receiver pool shrunk to {dst_blocks} blocks to fit", file=sys.stderr)
+    t0 = time.perf_counter()
+    src = fk.KVPool(layout, make_device_pool(geom, layout, pool_blocks, dev, seed=0))
+    dst = fk.KVPool(layout, make_device_pool(geom, layout, dst_blocks, dev, seed=1))
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t0
+    src_alloc = fk.Allocator(pool_blocks, fk.POLICY_SEGMENT, SEED_SRC_TABLE)
+    S = src_alloc.alloc(n)
+    dst_alloc = fk.Allocator(dst_blocks, POLICIES[args.dst_policy], SEED_DST_TABLE)
+    dst_alloc.mark_used(occupied_blocks(dst_blocks, 0.30, SEED_OCCUPANCY))
+    cfg = dict(threads=args.threads, unroll=args.unroll, grid=args.grid, cache=args.cache)
+    stream = torch.cuda.current_stream()
+
+    def step(events=None):
+        D = dst_alloc.alloc(n)
+        segs = fk.flowkv_plan(S, D, pool_blocks, dst_blocks)
+        segs_dev = fk.segments_to_device(segs, dev)
+        if events is not None:
+            events[0].record(stream)
+        fk.flowkv_transfer_ex(src, dst, segs_dev, len(segs), n, stream=stream, **cfg)
+        if events is not None:
+            events[1].record(stream)
+        dst_alloc.free(D)
+        return segs
+
+    segs = step()
+    torch.cuda.synchronize()
+    n_runs = len(segs)
+    # spot check of the measured configuration: a few moved blocks byte-equal
+    D_chk = dst_alloc.alloc(n)
+    dst_alloc.free(D_chk)
+    for i in (0, n // 2, n - 1):
+        if layout == fk.LAYOUT_BLOCK_MAJOR:
+            ok = torch.equal(src.tensors[0][int(S[i])], dst.tensors[0][int(D_chk[i])])
+        else:
+            ok = all(torch.equal(t_s[:, int(S[i])], t_d[:, int(D_chk[i])])
+                     for t_s, t_d in zip(src.tensors, dst.tensors))
+        assert ok, f"block {i} not moved"
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # ---- timed region -----------------------------------------------------------
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kern_ms = [a.elapsed_time(b) for a, b in evs]
+    kern_avg_ms = statistics.fmean(kern_ms)
+    ms_per_step = elapsed * 1e3 / args.steps
+    value = payload * args.steps / elapsed / 1e9
+    algo_bytes = 2 * payload + 16 * n_runs
+    achieved = algo_bytes / (kern_avg_ms * 1e-3) / 1e9
+
+    # ---- per-request latency: one request end to end, synchronised ----------------
+    lat = []
+    for _ in range(20):
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        step()
+        torch.cuda.synchronize()
+        lat.append((time.perf_counter() - t1) * 1e3)
+    ms_per_request = statistics.median(lat)
+
+    context = {}
+    if not args.no_context:
+        # kernel time with the 256 MB last-level cache flushed before each launch
+        scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        flushed = []
+        for _ in range(10):
+            scratch.fill_(1)
+            e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            step(e)
+            torch.cuda.synchronize()
+            flushed.append(e[0].elapsed_time(e[1]))
+        del scratch
+        # plain contiguous device-to-device copy of the same payload: the
+        # practical copy ceiling (also the HBM counter calibration kernel)
+        nbytes = int(args.calibrate_copy_gib * (1 << 30))
+        a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(10):
+            b.copy_(a)
+        e1.record()
+        torch.cuda.synchronize()
+        copy_ms = e0.elapsed_time(e1) / 10
+        del a, b
+        # the paper's block-wise pattern: one copy call per (block, layer, K/V)
+        # chunk, here as device-to-device copies of the same request
+        D = dst_alloc.alloc(n)
+        H = geom.chunk_bytes
+        t_chunks = time.perf_counter()
+        calls = 0
+        if layout == fk.LAYOUT_BLOCK_MAJOR:
+            sv = src.tensors[0].view(pool_blocks, 2 * geom.num_layers, -1)
+            dv = dst.tensors[0].view(dst_blocks, 2 * geom.num_layers, -1)
+            for i in range(n):
+                for r in range(2 * geom.num_layers):
+                    dv[int(D[i]), r].copy_(sv[int(S[i]), r])
+                    calls += 1
+        else:
+            for ts, td in zip(src.tensors, dst.tensors):
+                for kv in range(2):
+                    for i in range(n):
+                        td[kv, int(D[i])].copy_(ts[kv, int(S[i])])
+                        calls += 1
+        torch.cuda.synchronize()
+        per_chunk_ms = (time.perf_counter() - t_chunks) * 1e3
+        dst_alloc.free(D)
+        context = {
+            "kernel_ms_cache_flushed_median": round(statistics.median(flushed), 4),
+            "contiguous_copy_gbps": round(2 * nbytes / (copy_ms * 1e-3) / 1e9, 1),
+            "contiguous_copy_bytes": nbytes,
+            "per_chunk_copy_calls": calls,
+            "per_chunk_copy_ms": round(per_chunk_ms, 2),
+        }
+
+    # ---- CPU baseline: the oracle on the host ----------------------------------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        D = dst_alloc.alloc(n)
+        dst_alloc.free(D)
+        idx = torch.as_tensor(np.asarray(S, dtype=np.int64), device=dev)
+        slot = geom.slot_bytes
+        h_src = oracle.HostPool.zeros(layout, geom.num_layers, n, geom.block_size, slot)
+        if layout == fk.LAYOUT_BLOCK_MAJOR:
+            h_src.buffers[0][:] = src.tensors[0].index_select(0, idx).view(torch.uint8) \
+                .reshape(-1).cpu().numpy()
+        else:
+            for l, t in enumerate(src.tensors):
+                h_src.buffers[l][:] = t.index_select(1, idx).contiguous().view(torch.uint8) \
+                    .reshape(-1).cpu().numpy()
+        h_dst = oracle.HostPool.zeros(layout, geom.num_layers, n, geom.block_size, slot)
+        reps, t_cpu = 0, 0.0
+        while t_cpu < 10.0 and reps < 20:
+            t1 = time.perf_counter()
+            oracle.transfer_fast(h_src, h_dst, np.arange(n), np.arange(n))
+            t_cpu += time.perf_counter() - t1
+            reps += 1
+        cpu = {"value": round(payload * reps / t_cpu / 1e9, 3), "unit": "GB/s", "cores": 1,
+               "kind": "oracle",
+               "sample": f"the whole 813-block request ({payload} B), repeated {reps}x, "
+                         f"compact host pools of the moved blocks, numpy one thread; "
+                         f"{os.cpu_count()} host cores visible"}
+        del h_src, h_dst
+
+    traffic = traffic_from_profile(payload)
+    line = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic",
+        "config": {"workload": "llama3-8b-kv-13k-token-request", "layers": geom.num_layers,
+                   "kv_heads": geom.kv_heads, "head_dim": geom.head_dim,
+                   "block_size": geom.block_size, "kv_dtype": "bf16", "blocks": n,
+                   "payload_bytes": payload, "pool_blocks": [pool_blocks, dst_blocks],
+                   "layout": f"{args.layout}-major", "receiver_policy": args.dst_policy,
+                   "receiver_occupied": 0.30, "runs": n_runs},
+        "ms_per_request": round(ms_per_request, 4),
+        "pct_of_hbm_peak": round(100 * achieved / HBM_PEAK_GBPS, 2),
+        "kernel_ms_avg": round(kern_avg_ms, 4),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic},
+        "cpu_baseline": cpu,
+        "context": context,
+        "setup_s": round(setup_s, 2),
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,145 @@
+"""Shared plumbing for the GPU parity tests: pools on the device, downloads
+into the oracle's host pools, and the sampled comparison used at full size.
+
+Expected values always come from ``oracle`` run on host copies of device
+memory that the transfer kernel has not touched yet (the seeded source pool
+and the receiver's pre-image)."""
+
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2504_03775_amd import flowkv as fk
+from workloads import make_device_pool, pool_bytes, sample_indices
+
+LM, BM = fk.LAYOUT_LAYER_MAJOR, fk.LAYOUT_BLOCK_MAJOR
+
+
+def device_pool(geom, layout, num_blocks, seed):
+    ts = make_device_pool(geom, layout, num_blocks, "cuda", seed)
+    return fk.KVPool(layout, ts)
+
+
+def download_blocks(pool: fk.KVPool, ids) -> oracle.HostPool:
+    """Blocks `ids` of a device pool as a compact oracle pool of len(ids) blocks
+    (block i of the result = block ids[i] of the device pool), same layout."""
+    idx = torch.as_tensor(np.asarray(ids, dtype=np.int64), device=pool.device)
+    slot = pool.kv_heads * pool.head_dim * pool.elem_bytes
+    hp = oracle.HostPool.zeros(pool.layout, pool.num_layers, len(ids), pool.block_size, slot)
+    if len(ids) == 0:
+        return hp
+    # in pieces of at most ~256 MiB so full-size pools leave room for them
+    step = max(1, (256 << 20) // pool.block_bytes)
+    if pool.layout == BM:
+        out = hp.buffers[0].reshape(len(ids), -1)
+        for lo in range(0, len(ids), step):
+            sub = pool.tensors[0].index_select(0, idx[lo:lo + step]).contiguous()
+            out[lo:lo + step] = sub.view(torch.uint8).reshape(sub.shape[0], -1).cpu().numpy()
+    else:
+        for l, t in enumerate(pool.tensors):
+            out = hp.buffers[l].reshape(2, len(ids), -1)
+            for lo in range(0, len(ids), step):
+                sub = t.index_select(1, idx[lo:lo + step]).contiguous()
+                out[:, lo:lo + step] = sub.view(torch.uint8).reshape(2, sub.shape[1], -1).cpu().numpy()
+    return hp
+
+
+def download_all(pool: fk.KVPool) -> oracle.HostPool:
+    return download_blocks(pool, np.arange(pool.num_blocks))
+
+
+def host_equal(a: oracle.HostPool, b: oracle.HostPool) -> bool:
+    return all(np.array_equal(x, y) for x, y in zip(a.buffers, b.buffers))
+
+
+def first_mismatch(a: oracle.HostPool, b: oracle.HostPool):
+    for i, (x, y) in enumerate(zip(a.buffers, b.buffers)):
+        d = np.flatnonzero(x != y)
+        if d.size:
+            return i, int(d[0]), int(d.size)
+    return None
+
+
+def run_transfer(src, dst, segs, stream=None, **cfg):
+    total = fk.plan_total_blocks(segs)
+    dev = fk.segments_to_device(segs, src.device) if len(segs) else torch.zeros(
+        (0, 4), dtype=torch.int32, device=src.device)
+    if cfg:
+        fk.flowkv_transfer_ex(src, dst, dev, len(segs), total, stream=stream, **cfg)
+    else:
+        fk.flowkv_transfer(src, dst, dev, len(segs), total, stream=stream)
+    torch.cuda.synchronize()
+    return dev
+
+
+def plan_tables(tables, src_blocks, dst_blocks):
+    off = np.concatenate(([0], np.cumsum([len(s) for s, _ in tables]))).astype(np.int64)
+    S = np.concatenate([s for s, _ in tables]) if tables else np.zeros(0, np.int32)
+    D = np.concatenate([d for _, d in tables]) if tables else np.zeros(0, np.int32)
+    return fk.flowkv_plan_batch(off, S, D, src_blocks, dst_blocks), S, D
+
+
+def check_full_pool(geom, sl, dl, src_blocks, dst_blocks, tables, seed=0, **cfg):
+    """Whole-pool comparison (small pools): GPU result == oracle result."""
+    src = device_pool(geom, sl, src_blocks, seed)
+    dst = device_pool(geom, dl, dst_blocks, seed + 1)
+    h_src, h_dst = download_all(src), download_all(dst)
+    segs, S, D = plan_tables(tables, src_blocks, dst_blocks)
+    run_transfer(src, dst, segs, **cfg)
+    oracle.transfer_batch_fast(h_src, h_dst, [(s, d) for s, d in tables])
+    got = download_all(dst)
+    assert host_equal(got, h_dst), first_mismatch(got, h_dst)
+    return segs
+
+
+def check_sampled(wl, wl_ref, sl, dl, max_blocks=1536, untouched_frac=0.01, max_untouched=1024,
+                  seed_sample=7, **cfg):
+    """Full-size comparison on samples: a seeded sample of the moved blocks
+    (all of them when there are at most max_blocks) against the oracle, and
+    the guard blocks around every receiver run plus a seeded sample of the
+    other receiver blocks against their pre-image.
+
+    `wl` holds the block lists from the library's allocator (they drive the
+    device path), `wl_ref` the same workload from the oracle's allocator
+    (they pick what the oracle copies); the two must agree exactly."""
+    assert len(wl.tables) == len(wl_ref.tables)
+    for (s1, d1), (s2, d2) in zip(wl.tables, wl_ref.tables):
+        assert np.array_equal(s1, s2) and np.array_equal(d1, d2)
+    geom = wl.geom
+    need = pool_bytes(geom, wl.src_pool_blocks) + pool_bytes(geom, wl.dst_pool_blocks)
+    free, _ = torch.cuda.mem_get_info()
+    assert need < free, f"pools need {need / 2**30:.1f} GiB, {free / 2**30:.1f} GiB free"
+    src = device_pool(geom, sl, wl.src_pool_blocks, 0)
+    dst = device_pool(geom, dl, wl.dst_pool_blocks, 1)
+    segs, S, D = plan_tables(wl.tables, wl.src_pool_blocks, wl.dst_pool_blocks)
+    S_ref, D_ref = wl_ref.flat()
+    pick = sample_indices(len(S_ref), max_blocks, seed_sample)
+    h_src = download_blocks(src, S_ref[pick])
+    # receiver blocks not written: one guard on each side of every run, and a
+    # seeded sample of the rest
+    touched = np.zeros(wl.dst_pool_blocks, dtype=bool)
+    touched[D] = True
+    ends = segs["dst_block"] + segs["n_blocks"]
+    guards = np.concatenate((segs["dst_block"] - 1, ends))
+    guards = guards[(guards >= 0) & (guards < wl.dst_pool_blocks)]
+    guards = np.unique(guards[~touched[guards]])
+    rest = np.flatnonzero(~touched)
+    k = min(max_untouched, max(1, int(untouched_frac * rest.size))) if rest.size else 0
+    rest = rest[sample_indices(rest.size, k, seed_sample + 1)] if k else rest[:0]
+    keep = np.unique(np.concatenate((guards[:max_untouched], rest))).astype(np.int64)
+    before = download_blocks(dst, keep)
+    run_transfer(src, dst, segs, **cfg)
+    # oracle on compact pools: sampled logical block i moves from compact
+    # sender block i to compact receiver block i
+    expect = oracle.HostPool.zeros(dl, geom.num_layers, len(pick), geom.block_size,
+                                   geom.slot_bytes)
+    oracle.transfer_fast(h_src, expect, np.arange(len(pick)), np.arange(len(pick)))
+    got = download_blocks(dst, D_ref[pick])
+    assert host_equal(got, expect), first_mismatch(got, expect)
+    after = download_blocks(dst, keep)
+    assert host_equal(after, before), first_mismatch(after, before)
+    del src, dst
+    torch.cuda.empty_cache()
+    return segs, len(pick), len(keep)

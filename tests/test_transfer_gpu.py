@@ -1,0 +1,205 @@
+"""GPU parity: the one-launch transfer kernel against the oracle, byte-exact.
+
+Small pools are compared whole; the full-size workloads on seeded samples of
+the moved blocks, every guard block around a receiver run and a seeded 1%
+sample of the untouched receiver blocks.  Every case goes through the C ABI
+(allocator, planner, transfer) via the ctypes binding.
+"""
+
+import itertools
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2504_03775_amd import flowkv as fk
+from workloads import TINY, LLAMA3_8B, Geometry, random_table, recipes
+from tests.gpu_helpers import (BM, LM, check_full_pool, check_sampled, device_pool,
+                               download_all, host_equal, plan_tables, run_transfer)
+
+pytestmark = pytest.mark.gpu
+
+LAYOUT_PAIRS = list(itertools.product([LM, BM], [LM, BM]))
+NAMES = {LM: "layer", BM: "block"}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def lib_alloc(P, pol, seed):
+    return fk.Allocator(P, pol, seed)
+
+
+def ref_alloc(P, pol, seed):
+    return oracle.RefAllocator(P, pol, seed)
+
+
+@pytest.mark.parametrize("sl,dl", LAYOUT_PAIRS, ids=lambda x: NAMES[x])
+def test_tiny_full_pool_against_literal_loop(sl, dl):
+    wl = recipes.tiny()
+    say("tiny", NAMES[sl], NAMES[dl])
+    src = device_pool(wl.geom, sl, 64, 0)
+    dst = device_pool(wl.geom, dl, 64, 1)
+    h_src, h_dst = download_all(src), download_all(dst)
+    segs, S, D = plan_tables(wl.tables, 64, 64)
+    run_transfer(src, dst, segs)
+    oracle.transfer_ref(h_src, h_dst, S, D)  # the pure-Python definition
+    assert host_equal(download_all(dst), h_dst)
+    assert len(segs) == len(oracle.plan_ref(S.tolist(), D.tolist()))
+
+
+CONFIGS = [dict(), dict(threads=64), dict(threads=128, unroll=2), dict(threads=512, unroll=16),
+           dict(threads=1024, unroll=4), dict(grid=1), dict(grid=3, unroll=2),
+           dict(cache=1), dict(cache=2), dict(cache=3), dict(cache=4, unroll=16, grid=5)]
+
+
+def random_case(seed):
+    g = np.random.default_rng(seed)
+    L = int(g.choice([1, 2, 3, 7, 128]))
+    bs = int(g.choice([1, 2, 5, 16]))
+    hkv = int(g.choice([1, 2, 3]))
+    dh = int(g.choice([8, 40, 64, 128]))
+    geom = Geometry(f"rand{seed}", L, hkv, dh, bs, "float16")
+    if geom.chunk_bytes % 16:
+        geom = Geometry(f"rand{seed}", L, hkv, 64, bs, "float16")
+    # keep the pools small: at most ~48 MiB each
+    maxb = max(2, min(96, (48 << 20) // geom.block_bytes))
+    Bs = int(g.integers(1, maxb + 1))
+    Bd = int(g.integers(1, maxb + 1))
+    kind = g.integers(4)
+    n_req = int(g.integers(1, 4))
+    tables = []
+    if kind == 0:      # seeded permutations
+        ps, pd = g.permutation(Bs), g.permutation(Bd)
+    elif kind == 1:    # contiguous on both sides
+        ps, pd = np.arange(Bs), np.arange(Bd)
+    elif kind == 2:    # descending (never mergeable)
+        ps, pd = np.arange(Bs)[::-1], np.arange(Bd)[::-1]
+    else:              # ascending free blocks of a randomly occupied receiver
+        ps = np.arange(Bs)
+        busy = g.permutation(Bd)[: int(g.integers(0, Bd // 2 + 1))]
+        pd = np.setdiff1d(np.arange(Bd), busy)
+    n = int(g.integers(0, min(len(ps), len(pd)) + 1))
+    cuts = np.sort(g.integers(0, n + 1, size=n_req - 1))
+    bounds = np.concatenate(([0], cuts, [n]))
+    for i in range(n_req):
+        tables.append((ps[bounds[i]:bounds[i + 1]].astype(np.int32),
+                       pd[bounds[i]:bounds[i + 1]].astype(np.int32)))
+    return geom, Bs, Bd, tables
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_shapes_layouts_and_launch_shapes(seed):
+    geom, Bs, Bd, tables = random_case(seed)
+    sl, dl = LAYOUT_PAIRS[seed % 4]
+    cfg = CONFIGS[seed % len(CONFIGS)]
+    say(f"seed={seed} L={geom.num_layers} bs={geom.block_size} Hkv={geom.kv_heads} "
+        f"Dh={geom.head_dim} H={geom.chunk_bytes} Bs={Bs} Bd={Bd} "
+        f"n={sum(len(s) for s, _ in tables)} {NAMES[sl]}->{NAMES[dl]} cfg={cfg}")
+    check_full_pool(geom, sl, dl, Bs, Bd, tables, seed=seed, **cfg)
+
+
+def test_empty_plan_leaves_pool_unchanged():
+    src = device_pool(TINY, BM, 8, 0)
+    dst = device_pool(TINY, LM, 8, 1)
+    before = download_all(dst)
+    run_transfer(src, dst, fk.flowkv_plan([], [], 8, 8))
+    assert host_equal(download_all(dst), before)
+
+
+def test_last_block_ids_and_max_layers():
+    """Block IDs at the very end of the pools, 128 layers, per-lane path
+    (H = 16 * 3 * 40 * 2 = 3,840 bytes is not a multiple of the line)."""
+    geom = Geometry("edge", 128, 3, 40, 16, "bfloat16")
+    Bs, Bd = 9, 7
+    tables = [(np.array([8, 0, 7], np.int32), np.array([6, 5, 0], np.int32))]
+    for sl, dl in LAYOUT_PAIRS:
+        check_full_pool(geom, sl, dl, Bs, Bd, tables)
+
+
+def test_plan_records_outside_pools_are_skipped():
+    """A hand-made record pointing past the receiver pool moves nothing and
+    faults nothing; the valid record next to it still moves."""
+    geom = TINY
+    src = device_pool(geom, BM, 4, 0)
+    dst = device_pool(geom, BM, 4, 1)
+    h_src, h_dst = download_all(src), download_all(dst)
+    segs = np.zeros(2, dtype=fk.SEGMENT_DTYPE)
+    segs[0] = (1, 2, 1, 0)
+    segs[1] = (0, 3, 4, 1)  # blocks 3..6 of a 4-block receiver: out of range
+    dev = fk.segments_to_device(segs, src.device)
+    fk.flowkv_transfer(src, dst, dev, 2, 5)
+    torch.cuda.synchronize()
+    got = download_all(dst)
+    # record 0 moves block 1 -> 2; record 1's first block (0 -> 3) is inside
+    # both pools and moves, its other three blocks would land past the end
+    oracle.transfer_fast(h_src, h_dst, [1, 0], [2, 3])
+    assert host_equal(got, h_dst)
+
+
+def test_two_streams_two_plans():
+    """Two plans on two streams into disjoint receiver blocks."""
+    geom = LLAMA3_8B
+    src = device_pool(geom, BM, 16, 0)
+    dst = device_pool(geom, BM, 16, 1)
+    h_src, h_dst = download_all(src), download_all(dst)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    p1 = fk.flowkv_plan([0, 1, 2], [10, 11, 3], 16, 16)
+    p2 = fk.flowkv_plan([5, 9], [0, 1], 16, 16)
+    d1 = fk.segments_to_device(p1, src.device, s1)
+    d2 = fk.segments_to_device(p2, src.device, s2)
+    fk.flowkv_transfer(src, dst, d1, len(p1), 3, stream=s1)
+    fk.flowkv_transfer(src, dst, d2, len(p2), 2, stream=s2)
+    torch.cuda.synchronize()
+    oracle.transfer_fast(h_src, h_dst, [0, 1, 2, 5, 9], [10, 11, 3, 0, 1])
+    assert host_equal(download_all(dst), h_dst)
+
+
+# ---- full-size workloads -----------------------------------------------------
+
+def build(recipe, *args):
+    return recipe(lib_alloc, *args), recipe(ref_alloc, *args)
+
+
+@pytest.mark.parametrize("policy", ["fifo_sorted", "segment"])
+@pytest.mark.parametrize("sl,dl", [(BM, BM), (LM, LM), (LM, BM)], ids=lambda x: NAMES[x])
+def test_llama8b_13k_full_size(policy, sl, dl):
+    wl, ref = build(recipes.llama8b_13k, policy)
+    say(f"8b 13k {policy} {NAMES[sl]}->{NAMES[dl]}: {wl.n_blocks} blocks")
+    segs, nb, nk = check_sampled(wl, ref, sl, dl)
+    assert nb == 813  # every moved block checked
+    say(f"  {len(segs)} runs, {nb} blocks checked, {nk} untouched checked")
+
+
+@pytest.mark.parametrize("policy", ["segment", "fifo_shuffled"])
+def test_batch32_full_size(policy):
+    wl, ref = build(recipes.batch32, policy)
+    say(f"batch32 {policy}: {wl.n_blocks} blocks, pools {wl.src_pool_blocks}/{wl.dst_pool_blocks}")
+    segs, nb, nk = check_sampled(wl, ref, BM, BM)
+    if policy == "segment":
+        assert len(segs) == 32
+    say(f"  {len(segs)} runs, {nb} blocks checked")
+
+
+@pytest.mark.parametrize("policy,sl,dl", [("segment", BM, BM), ("fifo_shuffled", LM, LM)])
+def test_llama70b_tp8_full_size(policy, sl, dl):
+    wl, ref = build(recipes.llama70b_tp8, policy)
+    say(f"70b tp8 {policy} {NAMES[sl]}->{NAMES[dl]}: {wl.n_blocks} blocks")
+    segs, nb, nk = check_sampled(wl, ref, sl, dl, max_blocks=4096)
+    if policy == "segment":
+        assert len(segs) == 16
+    say(f"  {len(segs)} runs, {nb} blocks checked")
+
+
+@pytest.mark.parametrize("variant", ["segment", "shuffled", "stride2"])
+def test_churn_full_size(variant):
+    wl, ref = build(recipes.churn, variant)
+    say(f"churn {variant}: {wl.n_blocks} blocks")
+    segs, nb, nk = check_sampled(wl, ref, BM, BM)
+    if variant == "stride2":
+        assert len(segs) == wl.n_blocks
+    say(f"  {len(segs)} runs, {nb} blocks checked")
