@@ -6,7 +6,8 @@ A step is one pass of the whole hot path for one request:
      30%-occupied 65,536-block pool (host),
   2. bidirectional segment alignment of the sender's and receiver's block
      lists (host),
-  3. the plan is staged through pinned memory to the device (one small copy),
+  3. the plan is staged through a ring of pinned buffers to the device (one
+     small copy on a side stream, overlapping the previous step's kernel),
   4. one kernel launch moves every run's K and V of all 32 layers,
   5. the receiver's blocks are released again so every step sees the same
      pool state (host bookkeeping, after the launch).
@@ -24,6 +25,7 @@ the host.
 from __future__ import annotations
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -58,6 +60,8 @@ def parse():
     ap.add_argument("--cache", type=int, default=0)
     ap.add_argument("--calibrate-copy-gib", type=float, default=1.0,
                     help="size of the plain copy run beside the kernel (HBM counter scale)")
+    ap.add_argument("--calibration-only", action="store_true",
+                    help="of the context rows run only the plain copy (for counter runs)")
     return ap.parse_args()
 
 
@@ -122,15 +126,18 @@ def main():
     cfg = dict(threads=args.threads, unroll=args.unroll, grid=args.grid, cache=args.cache)
     stream = torch.cuda.current_stream()
 
+    stager = fk.PlanStager(dev, capacity=n)
+
     def step(events=None):
         D = dst_alloc.alloc(n)
         segs = fk.flowkv_plan(S, D, pool_blocks, dst_blocks)
-        segs_dev = fk.segments_to_device(segs, dev)
+        segs_dev = stager.stage(segs, stream)
         if events is not None:
             events[0].record(stream)
         fk.flowkv_transfer_ex(src, dst, segs_dev, len(segs), n, stream=stream, **cfg)
         if events is not None:
             events[1].record(stream)
+        stager.release(stream)
         dst_alloc.free(D)
         return segs
 
@@ -155,12 +162,18 @@ def main():
     # ---- timed region -----------------------------------------------------------
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(args.steps)]
+    # Python's cyclic garbage collector is run before and kept off during the
+    # timed steps (as timeit does): a full collection of the interpreter's
+    # heap can stall the host for tens of milliseconds mid-loop
+    gc.collect()
+    gc.disable()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         step(evs[i])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    gc.enable()
     kern_ms = [a.elapsed_time(b) for a, b in evs]
     kern_avg_ms = statistics.fmean(kern_ms)
     ms_per_step = elapsed * 1e3 / args.steps
@@ -183,7 +196,7 @@ def main():
         # kernel time with the 256 MB last-level cache flushed before each launch
         scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
         flushed = []
-        for _ in range(10):
+        for _ in range(0 if args.calibration_only else 10):
             scratch.fill_(1)
             e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
             step(e)
@@ -212,7 +225,9 @@ def main():
         H = geom.chunk_bytes
         t_chunks = time.perf_counter()
         calls = 0
-        if layout == fk.LAYOUT_BLOCK_MAJOR:
+        if args.calibration_only:
+            pass
+        elif layout == fk.LAYOUT_BLOCK_MAJOR:
             sv = src.tensors[0].view(pool_blocks, 2 * geom.num_layers, -1)
             dv = dst.tensors[0].view(dst_blocks, 2 * geom.num_layers, -1)
             for i in range(n):
@@ -229,7 +244,7 @@ def main():
         per_chunk_ms = (time.perf_counter() - t_chunks) * 1e3
         dst_alloc.free(D)
         context = {
-            "kernel_ms_cache_flushed_median": round(statistics.median(flushed), 4),
+            "kernel_ms_cache_flushed_median": round(statistics.median(flushed), 4) if flushed else None,
             "contiguous_copy_gbps": round(2 * nbytes / (copy_ms * 1e-3) / 1e9, 1),
             "contiguous_copy_bytes": nbytes,
             "per_chunk_copy_calls": calls,

@@ -85,11 +85,28 @@ SIGNATURES = {
 }
 
 
+def _hip_runtimes_loaded():
+    try:
+        maps = open("/proc/self/maps").read()
+    except OSError:
+        return []
+    return sorted({ln.split()[-1] for ln in maps.splitlines() if "libamdhip64" in ln})
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run paper_2504_03775_amd.build.build() "
                           "(or __graft_entry__.build()) first")
+    # The library must share PyTorch's HIP runtime: device pointers and stream
+    # handles come from torch.  Importing torch first loads its runtime, whose
+    # soname (libamdhip64.so.7) then satisfies the library's dependency; loading
+    # the library first would pull in a second runtime next to torch's.
+    import torch  # noqa: F401
+
     lib = ctypes.CDLL(LIB_PATH)
+    rts = _hip_runtimes_loaded()
+    if len(rts) > 1:
+        raise ImportError(f"two HIP runtimes loaded in one process: {rts}")
     for name, (res, args) in SIGNATURES.items():
         fn = getattr(lib, name)
         fn.restype = res
@@ -301,6 +318,68 @@ def segments_to_device(segs: np.ndarray, device, stream=None):
         return pinned.to(device, non_blocking=True)
     with torch.cuda.stream(stream):
         return pinned.to(device, non_blocking=True)
+
+
+class PlanStager:
+    """Ring of pinned host and device buffers for plans.
+
+    ``stage(segs, stream)`` copies a plan to the device on a side stream and
+    makes ``stream`` wait for that copy, so the upload overlaps whatever
+    ``stream`` is still running; ``release(stream)`` marks the slot busy until
+    ``stream`` passes the kernel that reads it.  A slot is reused only after
+    that (the host waits), so at most ``slots`` plans are in flight."""
+
+    def __init__(self, device, capacity: int = 4096, slots: int = 4):
+        import torch
+
+        self.device = torch.device(device)
+        self.slots = slots
+        self.capacity = 0
+        self.copy_stream = torch.cuda.Stream(self.device)
+        self.copied = [torch.cuda.Event() for _ in range(slots)]
+        self.done = [torch.cuda.Event() for _ in range(slots)]
+        self.used = [False] * slots
+        self.i = -1
+        self._grow(capacity)
+
+    def _grow(self, capacity: int):
+        import torch
+
+        torch.cuda.synchronize(self.device)
+        self.capacity = capacity
+        self.host = [torch.empty((capacity, 4), dtype=torch.int32, pin_memory=True)
+                     for _ in range(self.slots)]
+        self.dev = [torch.empty((capacity, 4), dtype=torch.int32, device=self.device)
+                    for _ in range(self.slots)]
+        self.used = [False] * self.slots
+
+    def stage(self, segs: np.ndarray, stream=None):
+        import torch
+
+        if stream is None:
+            stream = torch.cuda.current_stream(self.device)
+        k = len(segs)
+        if k > self.capacity:
+            self._grow(max(k, 2 * self.capacity))
+        self.i = (self.i + 1) % self.slots
+        j = self.i
+        if self.used[j]:
+            self.done[j].synchronize()
+        if k:
+            self.host[j].numpy()[:k] = np.ascontiguousarray(segs).view(np.int32).reshape(-1, 4)
+            with torch.cuda.stream(self.copy_stream):
+                self.dev[j][:k].copy_(self.host[j][:k], non_blocking=True)
+                self.copied[j].record(self.copy_stream)
+            stream.wait_event(self.copied[j])
+        self.used[j] = True
+        return self.dev[j][:k]
+
+    def release(self, stream=None):
+        import torch
+
+        if stream is None:
+            stream = torch.cuda.current_stream(self.device)
+        self.done[self.i].record(stream)
 
 
 def strerror(code: int) -> str:

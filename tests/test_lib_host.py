@@ -253,3 +253,9 @@ def test_transfer_rejects_bad_pools_without_touching_the_device():
     assert xfer(good_src, good_dst, segs=8) == fk.EINVAL  # misaligned plan
     assert xfer(good_src, good_dst, segs=0) == fk.EINVAL  # NULL plan
     assert xfer(good_src, good_dst, n_segs=-1) == fk.EINVAL
+
+
+def test_binding_shares_torchs_hip_runtime():
+    """Device pointers and streams come from torch, so the library must bind
+    to torch's HIP runtime: exactly one libamdhip64 may be mapped."""
+    assert len(fk._hip_runtimes_loaded()) == 1
