@@ -9,10 +9,11 @@
 //
 // Work decomposition.  A plan covers total_blocks logical blocks; block g's
 // bytes are split into tiles_per_block tiles, giving
-// units = total_blocks * tiles_per_block tiles.  Each workgroup takes a
-// contiguous range of units, finds the run holding its first block by binary
-// search over the runs' `first` fields, and then walks forward, so the run
-// lookup costs O(log runs) per workgroup plus one step per run crossed.
+// units = total_blocks * tiles_per_block tiles, walked grid-stride (by
+// default one tile per workgroup), so the workgroups resident at one moment
+// stream one window of neighbouring tiles.  A workgroup finds the run holding
+// its tile by a forward galloping search over the runs' `first` fields:
+// O(log runs) per jump, nothing while it stays inside a run.
 //
 // Addressing.  Within a block, byte offset o belongs to chunk r = o / H
 // (layer r / 2, K for even r, V for odd r) at offset o % H.  Block-major
@@ -52,7 +53,6 @@ struct XferArgs {
   int64_t chunk_bytes;      // H (bytes of one block/layer/K-or-V slab)
   int64_t block_bytes;      // BB = 2 * L * H
   int64_t units;            // total_blocks * tiles_per_block
-  int64_t units_per_wg;     // contiguous tiles per workgroup
   int32_t n_segs;
   int32_t num_layers;
   int32_t lines_per_chunk;  // H / line bytes (uniform path only)
@@ -67,9 +67,6 @@ struct XferArgs {
 // emit global (not flat) vector loads and stores with a scalar base.
 typedef __attribute__((address_space(1))) u32x4 gvec;
 
-__device__ __forceinline__ const gvec* as_global(const char* p) {
-  return (const gvec*)(p);
-}
 __device__ __forceinline__ gvec* as_global(char* p) { return (gvec*)(p); }
 
 typedef __attribute__((address_space(4))) const flowkv_segment cseg;
@@ -215,9 +212,10 @@ __global__ __launch_bounds__(1024) void kv_segment_copy(const XferArgs a) {
   __shared__ char* s_dst[kUniform ? 1 : FLOWKV_MAX_LAYERS];
   const int tid = threadIdx.x;
   const int64_t line = int64_t(blockDim.x) * 16;
-  int64_t u = int64_t(blockIdx.x) * a.units_per_wg;
-  const int64_t u_end = u + a.units_per_wg < a.units ? u + a.units_per_wg : a.units;
-  if (u >= u_end) return;  // uniform across the workgroup
+  // Grid-stride over tiles: the workgroups resident at any moment work on
+  // one window of neighbouring tiles (one tile per workgroup by default).
+  int64_t u = blockIdx.x;
+  if (u >= a.units) return;  // uniform across the workgroup
   if constexpr (!kUniform) {
     for (int l = tid; l < a.num_layers; l += blockDim.x) {
       s_src[l] = a.src.base[kSrcLM ? l : 0];
@@ -229,19 +227,32 @@ __global__ __launch_bounds__(1024) void kv_segment_copy(const XferArgs a) {
   // The plan is read-only for the whole launch: reading it through the
   // constant address space keeps the run lookups on the scalar unit.
   const cseg* segs = (const cseg*)(a.segs);
+  const int64_t stride = gridDim.x;
+  const int64_t g_step = stride / a.tiles_per_block;
+  const int32_t t_step = int32_t(stride - g_step * a.tiles_per_block);
   int64_t g = u / a.tiles_per_block;
   int32_t t = int32_t(u - g * a.tiles_per_block);
-  // the last run whose first block is <= g
-  int32_t lo = 0, hi = a.n_segs - 1;
-  while (lo < hi) {
-    const int32_t mid = (lo + hi + 1) >> 1;
-    if (segs[mid].first <= g) lo = mid;
-    else hi = mid - 1;
-  }
-  int32_t s = lo;
-  flowkv_segment seg = load_seg(segs + s);
-  for (; u < u_end; ++u) {
-    while (g - seg.first >= int64_t(seg.n_blocks) && s + 1 < a.n_segs) seg = load_seg(segs + ++s);
+  int32_t s = 0;
+  flowkv_segment seg = load_seg(segs);
+  for (; u < a.units; u += stride) {
+    if (g - seg.first >= int64_t(seg.n_blocks)) {
+      // g lies past run s: gallop forward for a bracket [lo, hi) with
+      // first[lo] <= g < first[hi], then bisect it to the last run whose
+      // first block is <= g
+      int32_t lo = s, hi = s + 1, step = 1;
+      while (hi < a.n_segs && segs[hi].first <= g) {
+        lo = hi;
+        step <<= 1;
+        hi = lo + step < a.n_segs ? lo + step : a.n_segs;
+      }
+      while (hi - lo > 1) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (segs[mid].first <= g) lo = mid;
+        else hi = mid;
+      }
+      s = lo;
+      seg = load_seg(segs + s);
+    }
     const int64_t off = g - seg.first;
     const int64_t sb = int64_t(seg.src_block) + off;
     const int64_t db = int64_t(seg.dst_block) + off;
@@ -254,8 +265,10 @@ __global__ __launch_bounds__(1024) void kv_segment_copy(const XferArgs a) {
       else
         copy_tile_lanes<kSrcLM, kDstLM, kU, kCache>(a, s_src, s_dst, sb, db, t, tid, line);
     }
-    if (++t == a.tiles_per_block) {
-      t = 0;
+    g += g_step;
+    t += t_step;
+    if (t >= a.tiles_per_block) {
+      t -= a.tiles_per_block;
       ++g;
     }
   }
@@ -295,14 +308,14 @@ KernelFn pick_kernel(bool src_lm, bool dst_lm, int unroll, int cache, bool unifo
   return pick_unroll<false, false>(unroll, cache, uniform);
 }
 
-// Library defaults, from a launch-shape sweep on the 13,000-token Llama-3-8B
-// request (threads x unroll x cache policy x grid): 512 threads moving 8
-// vectors each per tile (64 KiB tiles), nontemporal loads and
-// stores, four workgroups per CU.
+// Library defaults, from launch-shape sweeps (threads x unroll x cache
+// policy x grid) over the five transfer workloads: 512 threads moving 8
+// vectors each per tile (64 KiB tiles), nontemporal loads and stores, one
+// tile per workgroup.
 constexpr int kDefaultThreads = 512;
 constexpr int kDefaultUnroll = 8;
 constexpr int kDefaultCache = 4;  // nontemporal loads and stores
-constexpr int kWavesPerCU = 32;
+constexpr int64_t kMaxGridPerCU = 2048;
 
 std::atomic<int> g_cu_count[64];
 
@@ -435,16 +448,18 @@ extern "C" int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst
   }
   a.units = total_blocks * int64_t(a.tiles_per_block);
 
+  // default: one tile per workgroup, at most kMaxGridPerCU workgroups per CU
+  // (larger plans loop, grid stride)
+  int64_t launch = a.units;
   if (grid == 0) {
     int cus = 0;
     rc = cu_count(&cus);
     if (rc) return rc;
-    const int64_t per_cu = std::max<int64_t>(1, int64_t(kWavesPerCU) * 64 / threads);
-    grid = int(std::min<int64_t>(int64_t(cus) * per_cu, INT32_MAX));
+    launch = std::min<int64_t>(launch, int64_t(cus) * kMaxGridPerCU);
+  } else {
+    launch = std::min<int64_t>(launch, grid);
   }
-  const int64_t g = std::min<int64_t>(grid, a.units);
-  a.units_per_wg = (a.units + g - 1) / g;
-  const int64_t launch = (a.units + a.units_per_wg - 1) / a.units_per_wg;
+  launch = std::min<int64_t>(launch, INT32_MAX);
 
   KernelFn fn = pick_kernel(src->layout == FLOWKV_LAYOUT_LAYER_MAJOR,
                             dst->layout == FLOWKV_LAYOUT_LAYER_MAJOR, unroll, cache - 1, uniform);
