@@ -1,9 +1,11 @@
-"""Benchmark: one Llama-3-8B-shape 13,000-token request's KV cache moved
-between two paged pools on one MI355X.
+"""Benchmark of the KV-cache transfer hot path on one MI355X.
 
-A step is one pass of the whole hot path for one request:
+Default workload: one Llama-3-8B-shape request of 13,000 tokens (813 blocks
+of 2 MiB: 32 layers x K/V x 16 tokens x 8 KV heads x 128 dims, bf16) moved
+between two 65,536-block pools.  A step is one pass of the whole hot path for
+that request:
   1. the receiver's segment allocator places the request's 813 blocks in its
-     30%-occupied 65,536-block pool (host),
+     30%-occupied pool (host),
   2. bidirectional segment alignment of the sender's and receiver's block
      lists (host),
   3. the plan is staged through a ring of pinned buffers to the device (one
@@ -11,15 +13,18 @@ A step is one pass of the whole hot path for one request:
   4. one kernel launch moves every run's K and V of all 32 layers,
   5. the receiver's blocks are released again so every step sees the same
      pool state (host bookkeeping, after the launch).
-Steps are enqueued back to back on one stream; host work overlaps the
-previous step's kernel.  Inputs are resident in HBM before timing starts.
+The other workloads (--workload) take their block lists from the allocators
+at setup, as their recipes describe; their step is plan + stage + one launch
+for the whole batch.  Steps are enqueued back to back on one stream; host work
+overlaps the previous step's kernel.  Inputs are resident in HBM before timing
+starts.
 
 Prints one JSON line.  `value` is the effective transfer rate (payload bytes
 of K and V moved per second over the timed steps); `roofline` prices the
 transfer kernel's own launches (events around each launch on its stream)
 against the 8 TB/s HBM peak with 2x payload (read + write) of traffic;
-`cpu_baseline` is the oracle (numpy, one thread) moving the same request on
-the host.
+`cpu_baseline` is the oracle (numpy, one thread) moving the same blocks on the
+host.
 """
 
 from __future__ import annotations
@@ -42,15 +47,32 @@ METRIC = "effective KV transfer GB/s (% of HBM peak); ms per 13k-token request t
 KERNEL_SRC = os.path.join(ROOT, "paper_2504_03775_amd", "csrc", "flowkv_transfer.hip")
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "kv_segment_copy_llama3-8b-13k_pmc.txt")
 
+WORKLOADS = {
+    # name: (recipe, args, description)
+    "8b": ("llama8b_13k", (), "llama3-8b-kv-13k-token-request"),
+    "tiny": ("tiny", (), "tiny-2-layer-fp16-256-token-request"),
+    "batch": ("batch32", ("segment",), "llama3-8b-kv-batch-32-requests-2k-20k/segment-allocator"),
+    "batch-shuffled": ("batch32", ("fifo_shuffled",),
+                       "llama3-8b-kv-batch-32-requests-2k-20k/shuffled-free-list"),
+    "70b": ("llama70b_tp8", ("segment",), "llama3-70b-tp8-share-16x32k-tokens/segment-allocator"),
+    "70b-shuffled": ("llama70b_tp8", ("fifo_shuffled",),
+                     "llama3-70b-tp8-share-16x32k-tokens/shuffled-free-list"),
+    "churn": ("churn", ("segment",), "llama3-8b-kv-churn-128-live/segment-allocator"),
+    "churn-shuffled": ("churn", ("shuffled",), "llama3-8b-kv-churn-128-live/shuffled-free-list"),
+    "churn-stride2": ("churn", ("stride2",), "llama3-8b-kv-churn/stride-2-one-block-runs"),
+}
+
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="8b")
     ap.add_argument("--layout", choices=["block", "layer"], default="block",
                     help="pool layout of both sides: Eq. 5 block-major or per-layer")
-    ap.add_argument("--dst-policy", choices=["segment", "fifo_sorted"], default="segment")
+    ap.add_argument("--dst-policy", choices=["segment", "fifo_sorted"], default="segment",
+                    help="receiver allocator of the 8b workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-context", action="store_true",
                     help="skip the memcpy comparators and the flushed-cache timing")
@@ -69,7 +91,7 @@ def kernel_hash() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def traffic_from_profile(per_launch_payload: int):
+def traffic_from_profile():
     """HBM bytes per launch from the committed counter summary, scaled by the
     plain-copy calibration recorded with it; None if absent or if the kernel
     source changed since the counters were taken."""
@@ -94,43 +116,75 @@ def main():
     import torch
 
     from paper_2504_03775_amd import flowkv as fk
-    from workloads import (LLAMA3_8B, SEED_DST_TABLE, SEED_OCCUPANCY, SEED_SRC_TABLE,
-                           blocks_for, make_device_pool, occupied_blocks)
+    from workloads import (SEED_DST_TABLE, SEED_OCCUPANCY, make_device_pool,
+                           occupied_blocks, recipes)
     from workloads.recipes import POLICIES
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    geom = LLAMA3_8B
-    tokens, pool_blocks = 13_000, 65_536
-    n = blocks_for(tokens, geom.block_size)
     layout = fk.LAYOUT_BLOCK_MAJOR if args.layout == "block" else fk.LAYOUT_LAYER_MAJOR
-    payload = n * geom.block_bytes
+    single = args.workload == "8b"
 
-    # ---- setup (untimed): pools, sender's list, receiver's allocator ----------
-    free, total = torch.cuda.mem_get_info()
-    need = 2 * pool_blocks * geom.block_bytes
-    dst_blocks = pool_blocks
+    # ---- setup (untimed): block lists, pools ------------------------------------
+    make_alloc = lambda P, pol, seed: fk.Allocator(P, pol, seed)  # noqa: E731
+    recipe, rargs, wl_desc = WORKLOADS[args.workload]
+    if single:
+        wl = recipes.llama8b_13k(make_alloc, args.dst_policy)
+    elif recipe == "tiny":
+        wl = recipes.tiny()
+    else:
+        wl = getattr(recipes, recipe)(make_alloc, *rargs)
+    geom = wl.geom
+    S_all, D_all = wl.flat()
+    n = len(S_all)
+    offsets = wl.offsets()
+    payload = n * geom.block_bytes
+    src_blocks, dst_blocks = wl.src_pool_blocks, wl.dst_pool_blocks
+
+    free, _ = torch.cuda.mem_get_info()
+    need = (src_blocks + dst_blocks) * geom.block_bytes
     if need > free - (4 << 30):
-        dst_blocks = int(((free - (4 << 30)) // geom.block_bytes - pool_blocks) // 4096 * 4096)
-        print(f"note: receiver pool shrunk to {dst_blocks} blocks to fit", file=sys.stderr)
+        raise SystemExit(f"pools need {need / 2**30:.1f} GiB, {free / 2**30:.1f} GiB free")
     t0 = time.perf_counter()
-    src = fk.KVPool(layout, make_device_pool(geom, layout, pool_blocks, dev, seed=0))
+    src = fk.KVPool(layout, make_device_pool(geom, layout, src_blocks, dev, seed=0))
     dst = fk.KVPool(layout, make_device_pool(geom, layout, dst_blocks, dev, seed=1))
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t0
-    src_alloc = fk.Allocator(pool_blocks, fk.POLICY_SEGMENT, SEED_SRC_TABLE)
-    S = src_alloc.alloc(n)
-    dst_alloc = fk.Allocator(dst_blocks, POLICIES[args.dst_policy], SEED_DST_TABLE)
-    dst_alloc.mark_used(occupied_blocks(dst_blocks, 0.30, SEED_OCCUPANCY))
     cfg = dict(threads=args.threads, unroll=args.unroll, grid=args.grid, cache=args.cache)
     stream = torch.cuda.current_stream()
+    stager = fk.PlanStager(dev, capacity=max(1, n))
 
-    stager = fk.PlanStager(dev, capacity=n)
+    if single:
+        # the receiver's allocator runs inside every step: same occupancy as the
+        # recipe, the request's blocks taken and released each step
+        dst_alloc = fk.Allocator(dst_blocks, POLICIES[args.dst_policy], SEED_DST_TABLE)
+        dst_alloc.mark_used(occupied_blocks(dst_blocks, 0.30, SEED_OCCUPANCY))
+
+        def make_plan():
+            D = dst_alloc.alloc(n)
+            segs = fk.flowkv_plan(S_all, D, src_blocks, dst_blocks)
+            return segs, D
+
+        def after_launch(D):
+            dst_alloc.free(D)
+
+        def receiver_list():
+            D = dst_alloc.alloc(n)
+            dst_alloc.free(D)
+            return D
+    else:
+        def make_plan():
+            return fk.flowkv_plan_batch(offsets, S_all, D_all, src_blocks, dst_blocks), None
+
+        def after_launch(_):
+            pass
+
+        def receiver_list():
+            return D_all
 
     def step(events=None):
-        D = dst_alloc.alloc(n)
-        segs = fk.flowkv_plan(S, D, pool_blocks, dst_blocks)
+        segs, token = make_plan()
         segs_dev = stager.stage(segs, stream)
         if events is not None:
             events[0].record(stream)
@@ -138,20 +192,19 @@ def main():
         if events is not None:
             events[1].record(stream)
         stager.release(stream)
-        dst_alloc.free(D)
+        after_launch(token)
         return segs
 
     segs = step()
     torch.cuda.synchronize()
     n_runs = len(segs)
     # spot check of the measured configuration: a few moved blocks byte-equal
-    D_chk = dst_alloc.alloc(n)
-    dst_alloc.free(D_chk)
-    for i in (0, n // 2, n - 1):
+    D_chk = receiver_list()
+    for i in sorted({0, n // 2, n - 1}):
         if layout == fk.LAYOUT_BLOCK_MAJOR:
-            ok = torch.equal(src.tensors[0][int(S[i])], dst.tensors[0][int(D_chk[i])])
+            ok = torch.equal(src.tensors[0][int(S_all[i])], dst.tensors[0][int(D_chk[i])])
         else:
-            ok = all(torch.equal(t_s[:, int(S[i])], t_d[:, int(D_chk[i])])
+            ok = all(torch.equal(t_s[:, int(S_all[i])], t_d[:, int(D_chk[i])])
                      for t_s, t_d in zip(src.tensors, dst.tensors))
         assert ok, f"block {i} not moved"
 
@@ -181,7 +234,7 @@ def main():
     algo_bytes = 2 * payload + 16 * n_runs
     achieved = algo_bytes / (kern_avg_ms * 1e-3) / 1e9
 
-    # ---- per-request latency: one request end to end, synchronised ----------------
+    # ---- latency: one plan end to end, synchronised --------------------------------
     lat = []
     for _ in range(20):
         torch.cuda.synchronize()
@@ -189,22 +242,23 @@ def main():
         step()
         torch.cuda.synchronize()
         lat.append((time.perf_counter() - t1) * 1e3)
-    ms_per_request = statistics.median(lat)
+    ms_latency = statistics.median(lat)
 
     context = {}
     if not args.no_context:
         # kernel time with the 256 MB last-level cache flushed before each launch
-        scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
         flushed = []
-        for _ in range(0 if args.calibration_only else 10):
-            scratch.fill_(1)
-            e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-            step(e)
-            torch.cuda.synchronize()
-            flushed.append(e[0].elapsed_time(e[1]))
-        del scratch
-        # plain contiguous device-to-device copy of the same payload: the
-        # practical copy ceiling (also the HBM counter calibration kernel)
+        if not args.calibration_only:
+            scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+            for _ in range(10):
+                scratch.fill_(1)
+                e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                step(e)
+                torch.cuda.synchronize()
+                flushed.append(e[0].elapsed_time(e[1]))
+            del scratch
+        # plain contiguous device-to-device copy: the practical copy ceiling
+        # (also the HBM counter calibration kernel)
         nbytes = int(args.calibrate_copy_gib * (1 << 30))
         a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
         b = torch.empty_like(a)
@@ -219,48 +273,45 @@ def main():
         torch.cuda.synchronize()
         copy_ms = e0.elapsed_time(e1) / 10
         del a, b
-        # the paper's block-wise pattern: one copy call per (block, layer, K/V)
-        # chunk, here as device-to-device copies of the same request
-        D = dst_alloc.alloc(n)
-        H = geom.chunk_bytes
-        t_chunks = time.perf_counter()
-        calls = 0
-        if args.calibration_only:
-            pass
-        elif layout == fk.LAYOUT_BLOCK_MAJOR:
-            sv = src.tensors[0].view(pool_blocks, 2 * geom.num_layers, -1)
-            dv = dst.tensors[0].view(dst_blocks, 2 * geom.num_layers, -1)
-            for i in range(n):
-                for r in range(2 * geom.num_layers):
-                    dv[int(D[i]), r].copy_(sv[int(S[i]), r])
-                    calls += 1
-        else:
-            for ts, td in zip(src.tensors, dst.tensors):
-                for kv in range(2):
-                    for i in range(n):
-                        td[kv, int(D[i])].copy_(ts[kv, int(S[i])])
-                        calls += 1
-        torch.cuda.synchronize()
-        per_chunk_ms = (time.perf_counter() - t_chunks) * 1e3
-        dst_alloc.free(D)
         context = {
             "kernel_ms_cache_flushed_median": round(statistics.median(flushed), 4) if flushed else None,
             "contiguous_copy_gbps": round(2 * nbytes / (copy_ms * 1e-3) / 1e9, 1),
             "contiguous_copy_bytes": nbytes,
-            "per_chunk_copy_calls": calls,
-            "per_chunk_copy_ms": round(per_chunk_ms, 2),
         }
+        # the paper's block-wise pattern: one copy call per (block, layer, K/V)
+        # chunk, here as device-to-device copies of the same request
+        if single and not args.calibration_only:
+            D = receiver_list()
+            t_chunks = time.perf_counter()
+            calls = 0
+            if layout == fk.LAYOUT_BLOCK_MAJOR:
+                sv = src.tensors[0].view(src_blocks, 2 * geom.num_layers, -1)
+                dv = dst.tensors[0].view(dst_blocks, 2 * geom.num_layers, -1)
+                for i in range(n):
+                    for r in range(2 * geom.num_layers):
+                        dv[int(D[i]), r].copy_(sv[int(S_all[i]), r])
+                        calls += 1
+            else:
+                for ts, td in zip(src.tensors, dst.tensors):
+                    for kv in range(2):
+                        for i in range(n):
+                            td[kv, int(D[i])].copy_(ts[kv, int(S_all[i])])
+                            calls += 1
+            torch.cuda.synchronize()
+            context["per_chunk_copy_calls"] = calls
+            context["per_chunk_copy_ms"] = round((time.perf_counter() - t_chunks) * 1e3, 2)
 
     # ---- CPU baseline: the oracle on the host ----------------------------------------
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
 
-        D = dst_alloc.alloc(n)
-        dst_alloc.free(D)
-        idx = torch.as_tensor(np.asarray(S, dtype=np.int64), device=dev)
+        # a bounded sample: at most 813 blocks (one 13k-token request's worth)
+        k = min(n, 813)
+        pick = np.linspace(0, n - 1, k).round().astype(np.int64) if n > k else np.arange(n)
+        idx = torch.as_tensor(S_all[pick].astype(np.int64), device=dev)
         slot = geom.slot_bytes
-        h_src = oracle.HostPool.zeros(layout, geom.num_layers, n, geom.block_size, slot)
+        h_src = oracle.HostPool.zeros(layout, geom.num_layers, k, geom.block_size, slot)
         if layout == fk.LAYOUT_BLOCK_MAJOR:
             h_src.buffers[0][:] = src.tensors[0].index_select(0, idx).view(torch.uint8) \
                 .reshape(-1).cpu().numpy()
@@ -268,21 +319,30 @@ def main():
             for l, t in enumerate(src.tensors):
                 h_src.buffers[l][:] = t.index_select(1, idx).contiguous().view(torch.uint8) \
                     .reshape(-1).cpu().numpy()
-        h_dst = oracle.HostPool.zeros(layout, geom.num_layers, n, geom.block_size, slot)
+        h_dst = oracle.HostPool.zeros(layout, geom.num_layers, k, geom.block_size, slot)
         reps, t_cpu = 0, 0.0
         while t_cpu < 10.0 and reps < 20:
             t1 = time.perf_counter()
-            oracle.transfer_fast(h_src, h_dst, np.arange(n), np.arange(n))
+            oracle.transfer_fast(h_src, h_dst, np.arange(k), np.arange(k))
             t_cpu += time.perf_counter() - t1
             reps += 1
-        cpu = {"value": round(payload * reps / t_cpu / 1e9, 3), "unit": "GB/s", "cores": 1,
+        sample_bytes = k * geom.block_bytes
+        cpu = {"value": round(sample_bytes * reps / t_cpu / 1e9, 3), "unit": "GB/s", "cores": 1,
                "kind": "oracle",
-               "sample": f"the whole 813-block request ({payload} B), repeated {reps}x, "
-                         f"compact host pools of the moved blocks, numpy one thread; "
+               "sample": f"{k} of the workload's {n} blocks ({sample_bytes} B), repeated {reps}x, "
+                         f"compact host pools of those blocks, numpy one thread; "
                          f"{os.cpu_count()} host cores visible"}
         del h_src, h_dst
 
-    traffic = traffic_from_profile(payload)
+    traffic = traffic_from_profile() if (single and args.layout == "block") else None
+    kv_dtype = {"bfloat16": "bf16", "float16": "fp16"}[geom.dtype]
+    config = {"workload": wl_desc, "layers": geom.num_layers, "kv_heads": geom.kv_heads,
+              "head_dim": geom.head_dim, "block_size": geom.block_size, "kv_dtype": kv_dtype,
+              "requests": len(wl.tables), "blocks": n, "payload_bytes": payload,
+              "pool_blocks": [src_blocks, dst_blocks], "layout": f"{args.layout}-major",
+              "runs": n_runs}
+    if single:
+        config.update(receiver_policy=args.dst_policy, receiver_occupied=0.30)
     line = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -296,13 +356,8 @@ def main():
         "vs_baseline": None,
         "dtype": "u8",
         "data": "synthetic",
-        "config": {"workload": "llama3-8b-kv-13k-token-request", "layers": geom.num_layers,
-                   "kv_heads": geom.kv_heads, "head_dim": geom.head_dim,
-                   "block_size": geom.block_size, "kv_dtype": "bf16", "blocks": n,
-                   "payload_bytes": payload, "pool_blocks": [pool_blocks, dst_blocks],
-                   "layout": f"{args.layout}-major", "receiver_policy": args.dst_policy,
-                   "receiver_occupied": 0.30, "runs": n_runs},
-        "ms_per_request": round(ms_per_request, 4),
+        "config": config,
+        ("ms_per_request" if single else "ms_per_plan_latency"): round(ms_latency, 4),
         "pct_of_hbm_peak": round(100 * achieved / HBM_PEAK_GBPS, 2),
         "kernel_ms_avg": round(kern_avg_ms, 4),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,

@@ -120,12 +120,16 @@ typedef struct flowkv_pool {
    unroll:  16-byte vectors each thread moves per tile: 2, 4, 8 or 16.
    grid:    workgroups to launch, >= 1 (capped at the number of tiles).
    cache:   1 = plain loads and stores, 2 = nontemporal loads,
-            3 = nontemporal stores, 4 = nontemporal loads and stores. */
+            3 = nontemporal stores, 4 = nontemporal loads and stores.
+   order:   the order workgroups visit tiles in: 1 = plan order, 2 = blocks
+            scattered by a fixed permutation (a block's tiles stay together),
+            3 = tiles scattered by a fixed permutation.  Same result for all. */
 typedef struct flowkv_launch_config {
   int32_t threads;
   int32_t unroll;
   int32_t grid;
   int32_t cache;
+  int32_t order;
 } flowkv_launch_config;
 
 /* ---- allocator (section 3.3, allocator paragraph) -------------------------- */

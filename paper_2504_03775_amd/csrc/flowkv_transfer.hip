@@ -12,8 +12,9 @@
 // units = total_blocks * tiles_per_block tiles, walked grid-stride (by
 // default one tile per workgroup), so the workgroups resident at one moment
 // stream one window of neighbouring tiles.  A workgroup finds the run holding
-// its tile by a forward galloping search over the runs' `first` fields:
-// O(log runs) per jump, nothing while it stays inside a run.
+// its tile by a galloping search over the runs' `first` fields, starting
+// where equal-length runs would put it: O(log distance) per jump, nothing
+// while it stays inside a run.
 //
 // Addressing.  Within a block, byte offset o belongs to chunk r = o / H
 // (layer r / 2, K for even r, V for odd r) at offset o % H.  Block-major
@@ -53,6 +54,7 @@ struct XferArgs {
   int64_t chunk_bytes;      // H (bytes of one block/layer/K-or-V slab)
   int64_t block_bytes;      // BB = 2 * L * H
   int64_t units;            // total_blocks * tiles_per_block
+  int64_t total_blocks;     // blocks in the plan
   int32_t n_segs;
   int32_t num_layers;
   int32_t lines_per_chunk;  // H / line bytes (uniform path only)
@@ -60,7 +62,8 @@ struct XferArgs {
   int32_t tiles_per_block;  // ceil(lines_per_block / unroll)
   uint32_t h_magic;         // division by H (per-lane path)
   uint32_t h_shift;
-  int32_t pad;
+  int32_t order;            // 1 plan order, 2 blocks scattered, 3 tiles scattered
+  int64_t perm_mul;         // multiplier of the scattering permutation
 };
 
 // Pool memory is global memory; naming the address space lets the compiler
@@ -206,14 +209,52 @@ __device__ __forceinline__ void copy_tile_lanes(const XferArgs& a, char* const* 
   }
 }
 
+// Index of the last run whose first block is <= g, by galloping from run s
+// (backward or forward) to a bracket [lo, hi) with first[lo] <= g < first[hi]
+// and bisecting it.  Always returns an index in [0, n).
+__device__ __forceinline__ int32_t find_run(const cseg* segs, int32_t n, int64_t g, int32_t s) {
+  int32_t lo, hi, step = 1;
+  if (segs[s].first > g) {
+    hi = s;
+    lo = s - 1;
+    while (lo > 0 && segs[lo].first > g) {
+      hi = lo;
+      step <<= 1;
+      lo = hi - step > 0 ? hi - step : 0;
+    }
+    lo = lo > 0 ? lo : 0;
+  } else {
+    lo = s;
+    hi = s + 1;
+    while (hi < n && segs[hi].first <= g) {
+      lo = hi;
+      step <<= 1;
+      hi = lo + step < n ? lo + step : n;
+    }
+  }
+  while (hi - lo > 1) {
+    const int32_t mid = (lo + hi) >> 1;
+    if (segs[mid].first <= g) lo = mid;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// Where block g would sit if every run had the same length.
+__device__ __forceinline__ int32_t guess_run(const XferArgs& a, int64_t g) {
+  const int64_t s = g * a.n_segs / a.total_blocks;
+  return int32_t(s < a.n_segs ? s : a.n_segs - 1);
+}
+
 template <bool kSrcLM, bool kDstLM, int kU, int kCache, bool kUniform>
 __global__ __launch_bounds__(1024) void kv_segment_copy(const XferArgs a) {
   __shared__ char* s_src[kUniform ? 1 : FLOWKV_MAX_LAYERS];
   __shared__ char* s_dst[kUniform ? 1 : FLOWKV_MAX_LAYERS];
   const int tid = threadIdx.x;
   const int64_t line = int64_t(blockDim.x) * 16;
-  // Grid-stride over tiles: the workgroups resident at any moment work on
-  // one window of neighbouring tiles (one tile per workgroup by default).
+  // Grid-stride over tiles (one tile per workgroup by default).  In plan
+  // order the workgroups resident at one moment work on one window of
+  // neighbouring tiles; the scattered orders spread them over the plan.
   int64_t u = blockIdx.x;
   if (u >= a.units) return;  // uniform across the workgroup
   if constexpr (!kUniform) {
@@ -230,27 +271,25 @@ __global__ __launch_bounds__(1024) void kv_segment_copy(const XferArgs a) {
   const int64_t stride = gridDim.x;
   const int64_t g_step = stride / a.tiles_per_block;
   const int32_t t_step = int32_t(stride - g_step * a.tiles_per_block);
-  int64_t g = u / a.tiles_per_block;
-  int32_t t = int32_t(u - g * a.tiles_per_block);
-  int32_t s = 0;
-  flowkv_segment seg = load_seg(segs);
+  // (gl, tl): block and tile of tile u in plan order, stepped incrementally
+  int64_t gl = u / a.tiles_per_block;
+  int32_t tl = int32_t(u - gl * a.tiles_per_block);
+  int32_t s = -1;
+  flowkv_segment seg{};
   for (; u < a.units; u += stride) {
-    if (g - seg.first >= int64_t(seg.n_blocks)) {
-      // g lies past run s: gallop forward for a bracket [lo, hi) with
-      // first[lo] <= g < first[hi], then bisect it to the last run whose
-      // first block is <= g
-      int32_t lo = s, hi = s + 1, step = 1;
-      while (hi < a.n_segs && segs[hi].first <= g) {
-        lo = hi;
-        step <<= 1;
-        hi = lo + step < a.n_segs ? lo + step : a.n_segs;
-      }
-      while (hi - lo > 1) {
-        const int32_t mid = (lo + hi) >> 1;
-        if (segs[mid].first <= g) lo = mid;
-        else hi = mid;
-      }
-      s = lo;
+    // the tile this iteration visits: plan order, or a fixed permutation of
+    // blocks (2) or tiles (3) that scatters neighbouring workgroups
+    int64_t g = gl;
+    int32_t t = tl;
+    if (a.order == 2) {
+      g = gl * a.perm_mul % a.total_blocks;
+    } else if (a.order == 3) {
+      const int64_t v = u * a.perm_mul % a.units;
+      g = v / a.tiles_per_block;
+      t = int32_t(v - g * a.tiles_per_block);
+    }
+    if (s < 0 || g < seg.first || g - seg.first >= int64_t(seg.n_blocks)) {
+      s = find_run(segs, a.n_segs, g, (s < 0 || a.order != 1) ? guess_run(a, g) : s);
       seg = load_seg(segs + s);
     }
     const int64_t off = g - seg.first;
@@ -265,11 +304,11 @@ __global__ __launch_bounds__(1024) void kv_segment_copy(const XferArgs a) {
       else
         copy_tile_lanes<kSrcLM, kDstLM, kU, kCache>(a, s_src, s_dst, sb, db, t, tid, line);
     }
-    g += g_step;
-    t += t_step;
-    if (t >= a.tiles_per_block) {
-      t -= a.tiles_per_block;
-      ++g;
+    gl += g_step;
+    tl += t_step;
+    if (tl >= a.tiles_per_block) {
+      tl -= a.tiles_per_block;
+      ++gl;
     }
   }
 }
@@ -308,13 +347,18 @@ KernelFn pick_kernel(bool src_lm, bool dst_lm, int unroll, int cache, bool unifo
   return pick_unroll<false, false>(unroll, cache, uniform);
 }
 
-// Library defaults, from launch-shape sweeps (threads x unroll x cache
-// policy x grid) over the five transfer workloads: 512 threads moving 8
-// vectors each per tile (64 KiB tiles), nontemporal loads and stores, one
-// tile per workgroup.
-constexpr int kDefaultThreads = 512;
-constexpr int kDefaultUnroll = 8;
+// Library defaults, from interleaved launch-shape comparisons over the five
+// transfer workloads in both layouts: 1024 threads moving 4 vectors each per
+// tile (64 KiB tiles), nontemporal loads and stores, one tile per workgroup,
+// blocks visited in scattered order.  Scattering matters for block-major
+// pools holding long contiguous runs (the segment allocator's output): in
+// plan order the resident workgroups stream one contiguous window of each
+// pool, which ran 7-11% slower; for other plans it is neutral (within 1%).
+constexpr int kDefaultThreads = 1024;
+constexpr int kDefaultUnroll = 4;
 constexpr int kDefaultCache = 4;  // nontemporal loads and stores
+constexpr int kDefaultOrder = 2;  // blocks scattered
+constexpr uint64_t kPermPrime = 2654435761ull;
 constexpr int64_t kMaxGridPerCU = 2048;
 
 std::atomic<int> g_cu_count[64];
@@ -405,12 +449,15 @@ extern "C" int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst
     return fail(FLOWKV_EINVAL, "segment or block count above 2^31-1");
 
   int threads = kDefaultThreads, unroll = kDefaultUnroll, cache = kDefaultCache, grid = 0;
+  int order = kDefaultOrder;
   if (cfg) {
     if (cfg->threads) threads = cfg->threads;
     if (cfg->unroll) unroll = cfg->unroll;
     if (cfg->cache) cache = cfg->cache;
+    if (cfg->order) order = cfg->order;
     grid = cfg->grid;
   }
+  if (order < 1 || order > 3) return fail(FLOWKV_EINVAL, "order %d: need 1..3", order);
   if (threads < 64 || threads > 1024 || threads % 64)
     return fail(FLOWKV_EINVAL, "threads %d: need a multiple of 64 in 64..1024", threads);
   if (unroll != 2 && unroll != 4 && unroll != 8 && unroll != 16)
@@ -447,6 +494,14 @@ extern "C" int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst
     a.h_magic = uint32_t((((uint64_t(1) << l) - h) << 32) / h + 1);
   }
   a.units = total_blocks * int64_t(a.tiles_per_block);
+  a.total_blocks = total_blocks;
+  // scattering permutation x -> x * m mod M over blocks (M = total_blocks) or
+  // tiles (M = units): m is a prime above 2^31 reduced mod M, so it is coprime
+  // to every M < 2^31 and the map is a bijection; products stay below 2^62
+  a.order = order;
+  const int64_t perm_mod = order == 3 ? a.units : total_blocks;
+  if (order != 1 && perm_mod >= (int64_t(1) << 31)) a.order = 1;
+  a.perm_mul = int64_t(kPermPrime % uint64_t(perm_mod));
 
   // default: one tile per workgroup, at most kMaxGridPerCU workgroups per CU
   // (larger plans loop, grid stride)

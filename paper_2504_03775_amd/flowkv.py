@@ -53,7 +53,7 @@ class flowkv_pool(ctypes.Structure):
 
 class flowkv_launch_config(ctypes.Structure):
     _fields_ = [("threads", ctypes.c_int32), ("unroll", ctypes.c_int32),
-                ("grid", ctypes.c_int32), ("cache", ctypes.c_int32)]
+                ("grid", ctypes.c_int32), ("cache", ctypes.c_int32), ("order", ctypes.c_int32)]
 
 
 _I32P = ctypes.POINTER(ctypes.c_int32)
@@ -296,8 +296,8 @@ def flowkv_transfer(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_block
 
 def flowkv_transfer_ex(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_blocks: int,
                        threads: int = 0, unroll: int = 0, grid: int = 0, cache: int = 0,
-                       stream=None) -> None:
-    cfg = flowkv_launch_config(threads, unroll, grid, cache)
+                       order: int = 0, stream=None) -> None:
+    cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
     _check(_lib.flowkv_transfer_ex(ctypes.byref(src.desc), ctypes.byref(dst.desc),
                                    ctypes.c_void_p(segs_dev.data_ptr() if n_segs else 0),
                                    n_segs, total_blocks, ctypes.byref(cfg),

@@ -54,7 +54,9 @@ def test_tiny_full_pool_against_literal_loop(sl, dl):
 
 CONFIGS = [dict(), dict(threads=64), dict(threads=128, unroll=2), dict(threads=512, unroll=16),
            dict(threads=1024, unroll=4), dict(grid=1), dict(grid=3, unroll=2),
-           dict(cache=1), dict(cache=2), dict(cache=3), dict(cache=4, unroll=16, grid=5)]
+           dict(cache=1), dict(cache=2), dict(cache=3), dict(cache=4, unroll=16, grid=5),
+           dict(order=2), dict(order=3), dict(order=2, grid=7, threads=256),
+           dict(order=3, grid=2, unroll=4), dict(order=1, grid=4)]
 
 
 def random_case(seed):
@@ -92,7 +94,7 @@ def random_case(seed):
     return geom, Bs, Bd, tables
 
 
-@pytest.mark.parametrize("seed", range(40))
+@pytest.mark.parametrize("seed", range(48))
 def test_random_shapes_layouts_and_launch_shapes(seed):
     geom, Bs, Bd, tables = random_case(seed)
     sl, dl = LAYOUT_PAIRS[seed % 4]
