@@ -1,0 +1,56 @@
+"""The benchmark harness: its one-line JSON contract (GPU, in this process, on
+the tiny workload) and its refusal of several GPUs (CPU)."""
+
+import contextlib
+import io
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_bench_refuses_more_than_one_gpu():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def run_bench(*args):
+    import bench
+
+    out = io.StringIO()
+    argv = sys.argv
+    sys.argv = ["bench.py", *args]
+    try:
+        with contextlib.redirect_stdout(out):
+            bench.main()
+    finally:
+        sys.argv = argv
+    lines = [l for l in out.getvalue().splitlines() if l.strip()]
+    assert len(lines) == 1, lines
+    return json.loads(lines[0])
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("layout", ["block", "layer"])
+def test_bench_line_contract_on_tiny(layout):
+    j = run_bench("--workload", "tiny", "--layout", layout, "--steps", "3", "--warmup", "1",
+                  "--no-context")
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
+                "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config",
+                "roofline", "cpu_baseline"):
+        assert key in j, key
+    assert j["n_gpus"] == 1 and j["steps"] == 3 and j["warmup"] == 1
+    assert j["value"] > 0 and j["ms_per_step"] > 0
+    assert j["config"]["workload"].startswith("tiny") and j["config"]["blocks"] == 16
+    rf = j["roofline"]
+    assert rf["bound"] == "hbm" and rf["peak"] == 8000.0 and rf["unit"] == "GB/s"
+    assert abs(rf["frac"] - rf["achieved"] / rf["peak"]) < 1e-3
+    cb = j["cpu_baseline"]
+    assert cb["kind"] == "oracle" and cb["cores"] >= 1 and cb["value"] > 0
