@@ -21,7 +21,8 @@ starts.
 
 Prints one JSON line.  `value` is the effective transfer rate (payload bytes
 of K and V moved per second over the timed steps); `roofline` prices the
-transfer kernel's own launches (events around each launch on its stream)
+transfer kernel's own launches (events around each launch -- or, with
+--layerwise, around each step's per-layer launches -- on their stream)
 against the 8 TB/s HBM peak with 2x payload (read + write) of traffic;
 `cpu_baseline` is the oracle (numpy, one thread) moving the same blocks on the
 host.
@@ -73,6 +74,9 @@ def parse():
                     help="pool layout of both sides: Eq. 5 block-major or per-layer")
     ap.add_argument("--dst-policy", choices=["segment", "fifo_sorted"], default="segment",
                     help="receiver allocator of the 8b workload")
+    ap.add_argument("--layerwise", action="store_true",
+                    help="move each plan as one launch per layer (the paper's layer-wise "
+                         "ablation) instead of one launch for all layers")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-context", action="store_true",
                     help="skip the memcpy comparators and the flushed-cache timing")
@@ -188,7 +192,12 @@ def main():
         segs_dev = stager.stage(segs, stream)
         if events is not None:
             events[0].record(stream)
-        fk.flowkv_transfer_ex(src, dst, segs_dev, len(segs), n, stream=stream, **cfg)
+        if args.layerwise:
+            for layer in range(geom.num_layers):
+                fk.flowkv_transfer_layers(src, dst, segs_dev, len(segs), n, layer, 1,
+                                          stream=stream, **cfg)
+        else:
+            fk.flowkv_transfer_ex(src, dst, segs_dev, len(segs), n, stream=stream, **cfg)
         if events is not None:
             events[1].record(stream)
         stager.release(stream)
@@ -334,7 +343,8 @@ def main():
                          f"{os.cpu_count()} host cores visible"}
         del h_src, h_dst
 
-    traffic = traffic_from_profile() if (single and args.layout == "block") else None
+    traffic = traffic_from_profile() if (single and args.layout == "block"
+                                         and not args.layerwise) else None
     kv_dtype = {"bfloat16": "bf16", "float16": "fp16"}[geom.dtype]
     config = {"workload": wl_desc, "layers": geom.num_layers, "kv_heads": geom.kv_heads,
               "head_dim": geom.head_dim, "block_size": geom.block_size, "kv_dtype": kv_dtype,
@@ -343,6 +353,8 @@ def main():
               "runs": n_runs}
     if single:
         config.update(receiver_policy=args.dst_policy, receiver_occupied=0.30)
+    if args.layerwise:
+        config.update(launches_per_step=geom.num_layers, mode="layer-wise")
     line = {
         "metric": METRIC,
         "value": round(value, 2),

@@ -218,6 +218,19 @@ int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst,
                        int64_t total_blocks, const flowkv_launch_config* cfg,
                        void* hip_stream);
 
+/* Layer-wise variant (section 4.4 and Table 3: the "FlowKV-Layerwise"
+   ablation, which moves the KV cache one layer at a time, as a sender that
+   streams layers while prefill still runs would).  Moves only layers
+   [layer_begin, layer_begin + layer_count) -- K and V -- of every run; other
+   layers of the receiver's blocks are left unchanged.  Calling it for every
+   layer, one launch each, gives the same bytes as one flowkv_transfer_ex.
+   layer_count == 0 is a no-op.  EINVAL additionally for a layer range outside
+   the pools; otherwise arguments and errors as for flowkv_transfer_ex. */
+int flowkv_transfer_layers(const flowkv_pool* src, const flowkv_pool* dst,
+                           const flowkv_segment* segs_dev, int64_t n_segs,
+                           int64_t total_blocks, int32_t layer_begin, int32_t layer_count,
+                           const flowkv_launch_config* cfg, void* hip_stream);
+
 /* ---- diagnostics ------------------------------------------------------------ */
 
 /* Static name of a status code. */

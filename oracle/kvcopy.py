@@ -108,14 +108,27 @@ def _check(src: HostPool, dst: HostPool, S: Sequence[int], D: Sequence[int]):
     return S, D
 
 
-def transfer_ref(src: HostPool, dst: HostPool, S: Sequence[int], D: Sequence[int]) -> None:
+def _layer_range(pool: HostPool, layers):
+    if layers is None:
+        return range(pool.num_layers)
+    layers = range(layers.start, layers.stop) if isinstance(layers, range) else layers
+    for l in layers:
+        if l < 0 or l >= pool.num_layers:
+            raise ValueError(f"layer {l} outside the pool's {pool.num_layers} layers")
+    return layers
+
+
+def transfer_ref(src: HostPool, dst: HostPool, S: Sequence[int], D: Sequence[int],
+                 layers=None) -> None:
     """The definition as a literal loop over (token slot, layer, K/V).
 
+    ``layers`` restricts the copy to those layers (the layer-at-a-time
+    transmission the paper's section 4.4 compares against); all by default.
     Pure Python: for small pools only (a few thousand slot copies)."""
     S, D = _check(src, dst, S, D)
     bs, sb = src.block_size, src.slot_bytes
     for t in range(len(S) * bs):
-        for l in range(src.num_layers):
+        for l in _layer_range(src, layers):
             for kv in (0, 1):
                 si, so = slot_address(src, int(S[t // bs]), l, kv, t % bs)
                 di, do = slot_address(dst, int(D[t // bs]), l, kv, t % bs)
@@ -131,14 +144,16 @@ def _slot_rows(pool: HostPool, blocks: np.ndarray, l: int, kv: int, slots: np.nd
     return 0, ((blocks * L + l) * 2 + kv) * bs + slots
 
 
-def transfer_fast(src: HostPool, dst: HostPool, S: Sequence[int], D: Sequence[int]) -> None:
+def transfer_fast(src: HostPool, dst: HostPool, S: Sequence[int], D: Sequence[int],
+                  layers=None) -> None:
     """The same definition, vectorised over the token axis for each (layer,
-    K/V) with numpy fancy indexing (one gather and one scatter per pair)."""
+    K/V) with numpy fancy indexing (one gather and one scatter per pair);
+    ``layers`` as for ``transfer_ref``."""
     S, D = _check(src, dst, S, D)
     bs, sb = src.block_size, src.slot_bytes
     t = np.arange(len(S) * bs, dtype=np.int64)
     sblk, dblk, slot = S[t // bs], D[t // bs], t % bs
-    for l in range(src.num_layers):
+    for l in _layer_range(src, layers):
         for kv in (0, 1):
             si, srows = _slot_rows(src, sblk, l, kv, slot)
             di, drows = _slot_rows(dst, dblk, l, kv, slot)

@@ -52,13 +52,16 @@ struct XferArgs {
   PoolArg dst;
   const flowkv_segment* segs;
   int64_t chunk_bytes;      // H (bytes of one block/layer/K-or-V slab)
-  int64_t block_bytes;      // BB = 2 * L * H
+  int64_t block_bytes;      // BB = 2 * L * H (block stride of a block-major pool)
+  int64_t span_bytes;       // bytes moved per block: 2 * layer_count * H
+  int64_t span_off;         // offset of the first moved layer in a block: 2 * layer0 * H
   int64_t units;            // total_blocks * tiles_per_block
   int64_t total_blocks;     // blocks in the plan
   int32_t n_segs;
   int32_t num_layers;
+  int32_t layer0;           // first layer moved
   int32_t lines_per_chunk;  // H / line bytes (uniform path only)
-  int32_t lines_per_block;  // ceil(BB / line bytes)
+  int32_t lines_per_block;  // ceil(span_bytes / line bytes)
   int32_t tiles_per_block;  // ceil(lines_per_block / unroll)
   uint32_t h_magic;         // division by H (per-lane path)
   uint32_t h_shift;
@@ -96,15 +99,17 @@ __device__ __forceinline__ void store16(gvec* p, u32x4 v) {
   else *p = v;
 }
 
-// Start of line j (0 <= j < lines_per_block) of block b when every line lies
-// in one chunk: chunk r = j / lines_per_chunk, line w = j % lines_per_chunk.
+// Start of line j (0 <= j < lines_per_block) of the moved span of block b
+// when every line lies in one chunk: chunk r = j / lines_per_chunk (counted
+// from layer0), line w = j % lines_per_chunk.
 template <bool kLM>
 __device__ __forceinline__ char* line_base(const PoolArg& p, const XferArgs& a, int64_t b,
                                            int32_t j, int32_t r, int32_t w, int64_t line) {
   if constexpr (kLM)
-    return p.base[r >> 1] + (int64_t(r & 1) * p.num_blocks + b) * a.chunk_bytes + int64_t(w) * line;
+    return p.base[a.layer0 + (r >> 1)] + (int64_t(r & 1) * p.num_blocks + b) * a.chunk_bytes +
+           int64_t(w) * line;
   else
-    return p.base[0] + b * a.block_bytes + int64_t(j) * line;
+    return p.base[0] + b * a.block_bytes + a.span_off + int64_t(j) * line;
 }
 
 // Tile t of a block when every line lies inside one chunk: all pointer
@@ -132,8 +137,8 @@ __device__ __forceinline__ void copy_tile_uniform(const XferArgs& a, int64_t sb,
     char* dbase[kU];
 #pragma unroll
     for (int i = 0; i < kU; ++i) {
-      sbase[i] = kSrcLM ? a.src.base[rr[i] >> 1] : a.src.base[0];
-      dbase[i] = kDstLM ? a.dst.base[rr[i] >> 1] : a.dst.base[0];
+      sbase[i] = kSrcLM ? a.src.base[a.layer0 + (rr[i] >> 1)] : a.src.base[0] + a.span_off;
+      dbase[i] = kDstLM ? a.dst.base[a.layer0 + (rr[i] >> 1)] : a.dst.base[0] + a.span_off;
     }
     const gvec* sp[kU];
     gvec* dp[kU];
@@ -168,16 +173,17 @@ __device__ __forceinline__ uint32_t div_by_h(uint32_t o, uint32_t magic, uint32_
   return uint32_t((hi + o) >> shift);
 }
 
-// Byte o of block b for any H (a multiple of 16): chunk r = o / H.
+// Byte o of the moved span of block b for any H (a multiple of 16): chunk
+// r = o / H, counted from layer0.
 template <bool kLM>
 __device__ __forceinline__ char* byte_addr(const PoolArg& p, char* const* lds_base,
                                            const XferArgs& a, int64_t b, int64_t o) {
   if constexpr (kLM) {
     const uint32_t r = div_by_h(uint32_t(o), a.h_magic, a.h_shift);
     const int64_t w = o - int64_t(r) * a.chunk_bytes;
-    return lds_base[r >> 1] + (int64_t(r & 1) * p.num_blocks + b) * a.chunk_bytes + w;
+    return lds_base[a.layer0 + (r >> 1)] + (int64_t(r & 1) * p.num_blocks + b) * a.chunk_bytes + w;
   } else {
-    return p.base[0] + b * a.block_bytes + o;
+    return p.base[0] + b * a.block_bytes + a.span_off + o;
   }
 }
 
@@ -187,7 +193,7 @@ __device__ __forceinline__ void copy_tile_lanes(const XferArgs& a, char* const* 
                                                 char* const* s_dst, int64_t sb, int64_t db,
                                                 int32_t t, int tid, int64_t line) {
   const int64_t o0 = int64_t(t) * kU * line + int64_t(tid) * 16;
-  if (int64_t(t + 1) * kU * line <= a.block_bytes) {
+  if (int64_t(t + 1) * kU * line <= a.span_bytes) {
     const gvec* sp[kU];
     gvec* dp[kU];
 #pragma unroll
@@ -202,7 +208,7 @@ __device__ __forceinline__ void copy_tile_lanes(const XferArgs& a, char* const* 
 #pragma unroll
     for (int i = 0; i < kU; ++i) store16<kCache>(dp[i], v[i]);
   } else {
-    for (int64_t o = o0; o < a.block_bytes; o += line) {
+    for (int64_t o = o0; o < a.span_bytes; o += line) {
       const u32x4 v = load16<kCache>(as_global(byte_addr<kSrcLM>(a.src, s_src, a, sb, o)));
       store16<kCache>(as_global(byte_addr<kDstLM>(a.dst, s_dst, a, db, o)), v);
     }
@@ -422,10 +428,12 @@ bool overlaps(const Range& x, const Range& y) { return x.lo < y.hi && y.lo < x.h
 
 }  // namespace
 
-extern "C" int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst,
-                                  const flowkv_segment* segs_dev, int64_t n_segs,
-                                  int64_t total_blocks, const flowkv_launch_config* cfg,
-                                  void* hip_stream) {
+namespace {
+
+int launch_transfer(const flowkv_pool* src, const flowkv_pool* dst,
+                    const flowkv_segment* segs_dev, int64_t n_segs, int64_t total_blocks,
+                    int32_t layer_begin, int32_t layer_count, bool whole,
+                    const flowkv_launch_config* cfg, void* hip_stream) {
   Range rs[FLOWKV_MAX_LAYERS], rd[FLOWKV_MAX_LAYERS];
   int ns = 0, nd = 0;
   int rc = pool_ranges(src, "sender", rs, &ns);
@@ -447,6 +455,13 @@ extern "C" int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst
     return fail(FLOWKV_EINVAL, "negative segment or block count");
   if (n_segs > INT32_MAX || total_blocks > INT32_MAX)
     return fail(FLOWKV_EINVAL, "segment or block count above 2^31-1");
+  if (whole) {
+    layer_begin = 0;
+    layer_count = src->num_layers;
+  }
+  if (layer_begin < 0 || layer_count < 0 || layer_begin + int64_t(layer_count) > src->num_layers)
+    return fail(FLOWKV_EINVAL, "layers [%d, %d + %d) outside the pools' %d layers", layer_begin,
+                layer_begin, layer_count, src->num_layers);
 
   int threads = kDefaultThreads, unroll = kDefaultUnroll, cache = kDefaultCache, grid = 0;
   int order = kDefaultOrder;
@@ -464,7 +479,7 @@ extern "C" int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst
     return fail(FLOWKV_EINVAL, "unroll %d: need 2, 4, 8 or 16", unroll);
   if (cache < 1 || cache > 4) return fail(FLOWKV_EINVAL, "cache %d: need 1..4", cache);
   if (grid < 0) return fail(FLOWKV_EINVAL, "negative grid %d", grid);
-  if (n_segs == 0 || total_blocks == 0) return ok();
+  if (n_segs == 0 || total_blocks == 0 || layer_count == 0) return ok();
   if (!segs_dev) return fail(FLOWKV_EINVAL, "NULL segment list");
   if (reinterpret_cast<uintptr_t>(segs_dev) % 16)
     return fail(FLOWKV_EINVAL, "segment list not 16-byte aligned");
@@ -479,10 +494,13 @@ extern "C" int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst
   a.num_layers = src->num_layers;
   a.chunk_bytes = src->chunk_bytes;
   a.block_bytes = 2 * int64_t(src->num_layers) * src->chunk_bytes;
+  a.layer0 = layer_begin;
+  a.span_off = 2 * int64_t(layer_begin) * src->chunk_bytes;
+  a.span_bytes = 2 * int64_t(layer_count) * src->chunk_bytes;
   const int64_t line = int64_t(threads) * 16;
   const bool uniform = a.chunk_bytes % line == 0;
   a.lines_per_chunk = uniform ? int32_t(a.chunk_bytes / line) : 0;
-  a.lines_per_block = int32_t((a.block_bytes + line - 1) / line);
+  a.lines_per_block = int32_t((a.span_bytes + line - 1) / line);
   a.tiles_per_block = (a.lines_per_block + unroll - 1) / unroll;
   // division by H for the per-lane path: l = ceil(log2 H),
   // m = floor(2^32 (2^l - H) / H) + 1, q = (umulhi(o, m) + o) >> l
@@ -525,6 +543,24 @@ extern "C" int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst
   if (e == hipSuccess) e = hipGetLastError();
   if (e != hipSuccess) return fail(FLOWKV_EHIP, "kernel launch: %s", hipGetErrorString(e));
   return ok();
+}
+
+}  // namespace
+
+extern "C" int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst,
+                                  const flowkv_segment* segs_dev, int64_t n_segs,
+                                  int64_t total_blocks, const flowkv_launch_config* cfg,
+                                  void* hip_stream) {
+  return launch_transfer(src, dst, segs_dev, n_segs, total_blocks, 0, 0, true, cfg, hip_stream);
+}
+
+extern "C" int flowkv_transfer_layers(const flowkv_pool* src, const flowkv_pool* dst,
+                                      const flowkv_segment* segs_dev, int64_t n_segs,
+                                      int64_t total_blocks, int32_t layer_begin,
+                                      int32_t layer_count, const flowkv_launch_config* cfg,
+                                      void* hip_stream) {
+  return launch_transfer(src, dst, segs_dev, n_segs, total_blocks, layer_begin, layer_count,
+                         false, cfg, hip_stream);
 }
 
 extern "C" int flowkv_transfer(const flowkv_pool* src, const flowkv_pool* dst,

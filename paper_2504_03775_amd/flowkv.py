@@ -80,6 +80,10 @@ SIGNATURES = {
     "flowkv_transfer_ex": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_int64,
                                           ctypes.c_int64, ctypes.POINTER(flowkv_launch_config),
                                           ctypes.c_void_p]),
+    "flowkv_transfer_layers": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_int64,
+                                              ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                              ctypes.POINTER(flowkv_launch_config),
+                                              ctypes.c_void_p]),
     "flowkv_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "flowkv_last_error": (ctypes.c_char_p, []),
 }
@@ -303,6 +307,18 @@ def flowkv_transfer_ex(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_bl
                                    n_segs, total_blocks, ctypes.byref(cfg),
                                    ctypes.c_void_p(_stream_handle(stream))),
            "flowkv_transfer_ex")
+
+
+def flowkv_transfer_layers(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_blocks: int,
+                           layer_begin: int, layer_count: int, threads: int = 0, unroll: int = 0,
+                           grid: int = 0, cache: int = 0, order: int = 0, stream=None) -> None:
+    """Enqueue the copy of layers [layer_begin, layer_begin + layer_count) only."""
+    cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
+    _check(_lib.flowkv_transfer_layers(ctypes.byref(src.desc), ctypes.byref(dst.desc),
+                                       ctypes.c_void_p(segs_dev.data_ptr() if n_segs else 0),
+                                       n_segs, total_blocks, layer_begin, layer_count,
+                                       ctypes.byref(cfg), ctypes.c_void_p(_stream_handle(stream))),
+           "flowkv_transfer_layers")
 
 
 def segments_to_device(segs: np.ndarray, device, stream=None):

@@ -251,6 +251,13 @@ def test_transfer_rejects_bad_pools_without_touching_the_device():
                 fk.flowkv_launch_config(256, 8, 0, 9), fk.flowkv_launch_config(256, 8, 0, 0, 4),
                 fk.flowkv_launch_config(256, 8, 0, 0, -1)):
         assert xfer(good_src, good_dst, n_segs=0, total=0, cfg=cfg) == fk.EINVAL
+    # layer ranges of the layer-wise entry point
+    def xfer_layers(l0, lc):
+        return fk.lib().flowkv_transfer_layers(ctypes.byref(good_src), ctypes.byref(good_dst),
+                                               ctypes.c_void_p(1 << 12), 1, 1, l0, lc, None, None)
+    for l0, lc in ((-1, 1), (0, 3), (2, 1), (1, 2), (0, -1)):
+        assert xfer_layers(l0, lc) == fk.EINVAL, (l0, lc)
+    assert xfer_layers(1, 0) == fk.OK  # nothing to move: no launch
     assert xfer(good_src, good_dst, segs=8) == fk.EINVAL  # misaligned plan
     assert xfer(good_src, good_dst, segs=0) == fk.EINVAL  # NULL plan
     assert xfer(good_src, good_dst, n_segs=-1) == fk.EINVAL

@@ -206,3 +206,48 @@ def test_loop_and_vectorised_forms_agree(data):
     transfer_fast(src, b, S, D)
     for x, y in zip(a.buffers, b.buffers):
         assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("sl,dl", list(itertools.product(LAYOUTS, LAYOUTS)))
+def test_layer_subset_moves_only_those_layers(sl, dl):
+    """The layer-at-a-time variant: a layer subset moves exactly those layers'
+    K and V slots; every other receiver slot keeps its tag."""
+    rng = np.random.default_rng(5)
+    L, bs, slot = 5, 2, 32
+    src = make_pool(sl, L, 7, bs, slot, 0x51C0)
+    dst = make_pool(dl, L, 8, bs, slot, 0xD57)
+    before = dst.copy()
+    S, D = rng.permutation(7)[:4], rng.permutation(8)[:4]
+    moved = [1, 3]
+    transfer_fast(src, dst, S, D, layers=moved)
+    vd, vb = shaped(dst), shaped(before)
+    Dmap = {int(d): int(s) for s, d in zip(S, D)}
+    for b in range(8):
+        for l in range(L):
+            for kv in (0, 1):
+                for s in range(bs):
+                    got = get_slot(dst, vd, b, l, kv, s)
+                    if b in Dmap and l in moved:
+                        assert tuple(got[:4]) == (Dmap[b], l, kv, s)
+                    else:
+                        assert np.array_equal(got, get_slot(before, vb, b, l, kv, s))
+
+
+@pytest.mark.parametrize("fn", [transfer_ref, transfer_fast])
+def test_layer_by_layer_composes_to_the_whole_transfer(fn):
+    rng = np.random.default_rng(9)
+    L, bs, slot = 4, 3, 16
+    src = HostPool.zeros(BLOCK_MAJOR, L, 6, bs, slot)
+    src.buffers[0][:] = rng.integers(0, 256, src.buffers[0].size, dtype=np.uint8)
+    dst = HostPool.zeros(LAYER_MAJOR, L, 6, bs, slot)
+    for buf in dst.buffers:
+        buf[:] = rng.integers(0, 256, buf.size, dtype=np.uint8)
+    S, D = rng.permutation(6)[:5], rng.permutation(6)[:5]
+    whole, parts = dst.copy(), dst.copy()
+    fn(src, whole, S, D)
+    for l in reversed(range(L)):
+        fn(src, parts, S, D, layers=[l])
+    for a, b in zip(whole.buffers, parts.buffers):
+        assert np.array_equal(a, b)
+    with pytest.raises(ValueError):
+        fn(src, parts, S, D, layers=[L])

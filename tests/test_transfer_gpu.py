@@ -205,3 +205,45 @@ def test_churn_full_size(variant):
     if variant == "stride2":
         assert len(segs) == wl.n_blocks
     say(f"  {len(segs)} runs, {nb} blocks checked")
+
+
+# ---- layer-wise variant (section 4.4, Table 3: FlowKV-Layerwise) -------------
+
+@pytest.mark.parametrize("seed", range(16))
+def test_layer_ranges_against_oracle(seed):
+    geom, Bs, Bd, tables = random_case(1000 + seed)
+    sl, dl = LAYOUT_PAIRS[seed % 4]
+    g = np.random.default_rng(seed)
+    l0 = int(g.integers(0, geom.num_layers))
+    lc = int(g.integers(1, geom.num_layers - l0 + 1))
+    cfg = CONFIGS[seed % len(CONFIGS)]
+    say(f"layers seed={seed} L={geom.num_layers} [{l0}, {l0 + lc}) H={geom.chunk_bytes} "
+        f"{NAMES[sl]}->{NAMES[dl]} cfg={cfg}")
+    src = device_pool(geom, sl, Bs, seed)
+    dst = device_pool(geom, dl, Bd, seed + 1)
+    h_src, h_dst = download_all(src), download_all(dst)
+    segs, S, D = plan_tables(tables, Bs, Bd)
+    dev = fk.segments_to_device(segs, src.device) if len(segs) else torch.zeros(
+        (0, 4), dtype=torch.int32, device=src.device)
+    fk.flowkv_transfer_layers(src, dst, dev, len(segs), fk.plan_total_blocks(segs), l0, lc, **cfg)
+    torch.cuda.synchronize()
+    for s_, d_ in tables:
+        oracle.transfer_fast(h_src, h_dst, s_, d_, layers=range(l0, l0 + lc))
+    assert host_equal(download_all(dst), h_dst)
+
+
+@pytest.mark.parametrize("sl,dl", [(BM, BM), (LM, LM)], ids=lambda x: NAMES[x])
+def test_one_launch_per_layer_equals_one_launch(sl, dl):
+    """The 8B geometry (32 layers): 32 per-layer launches give the same
+    receiver pool as one whole-plan launch."""
+    geom = LLAMA3_8B
+    src = device_pool(geom, sl, 24, 0)
+    d1 = device_pool(geom, dl, 24, 1)
+    d2 = device_pool(geom, dl, 24, 1)
+    segs = fk.flowkv_plan([3, 4, 5, 9, 1], [0, 1, 2, 20, 7], 24, 24)
+    dev = fk.segments_to_device(segs, src.device)
+    fk.flowkv_transfer(src, d1, dev, len(segs), 5)
+    for l in range(geom.num_layers):
+        fk.flowkv_transfer_layers(src, d2, dev, len(segs), 5, l, 1)
+    torch.cuda.synchronize()
+    assert host_equal(download_all(d1), download_all(d2))
