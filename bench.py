@@ -8,8 +8,9 @@ that request:
      30%-occupied pool (host),
   2. bidirectional segment alignment of the sender's and receiver's block
      lists (host),
-  3. the plan is staged through a ring of pinned buffers to the device (one
-     small copy on a side stream, overlapping the previous step's kernel),
+  3. the plan goes to the device: in the kernel's arguments when it has at
+     most 64 runs (it has 43), else staged through a ring of pinned buffers
+     (one small copy on a side stream, overlapping the previous kernel),
   4. one kernel launch moves every run's K and V of all 32 layers,
   5. the receiver's blocks are released again so every step sees the same
      pool state (host bookkeeping, after the launch).
@@ -77,6 +78,8 @@ def parse():
     ap.add_argument("--layerwise", action="store_true",
                     help="move each plan as one launch per layer (the paper's layer-wise "
                          "ablation) instead of one launch for all layers")
+    ap.add_argument("--staged-plan", action="store_true",
+                    help="always stage the plan in device memory (no kernel-argument plans)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-context", action="store_true",
                     help="skip the memcpy comparators and the flushed-cache timing")
@@ -189,10 +192,14 @@ def main():
 
     def step(events=None):
         segs, token = make_plan()
-        segs_dev = stager.stage(segs, stream)
+        # small plans ride in the kernel arguments; longer ones are staged
+        inline = len(segs) <= fk.INLINE_RUNS and not args.layerwise and not args.staged_plan
+        segs_dev = None if inline else stager.stage(segs, stream)
         if events is not None:
             events[0].record(stream)
-        if args.layerwise:
+        if inline:
+            fk.flowkv_transfer_inline(src, dst, segs, n, stream=stream, **cfg)
+        elif args.layerwise:
             for layer in range(geom.num_layers):
                 fk.flowkv_transfer_layers(src, dst, segs_dev, len(segs), n, layer, 1,
                                           stream=stream, **cfg)
@@ -200,7 +207,8 @@ def main():
             fk.flowkv_transfer_ex(src, dst, segs_dev, len(segs), n, stream=stream, **cfg)
         if events is not None:
             events[1].record(stream)
-        stager.release(stream)
+        if not inline:
+            stager.release(stream)
         after_launch(token)
         return segs
 
@@ -355,6 +363,8 @@ def main():
         config.update(receiver_policy=args.dst_policy, receiver_occupied=0.30)
     if args.layerwise:
         config.update(launches_per_step=geom.num_layers, mode="layer-wise")
+    config["plan_in"] = ("kernel-arguments" if n_runs <= fk.INLINE_RUNS and not args.layerwise
+                         and not args.staged_plan else "device-memory")
     line = {
         "metric": METRIC,
         "value": round(value, 2),

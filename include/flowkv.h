@@ -79,6 +79,7 @@ enum {
 };
 
 #define FLOWKV_MAX_LAYERS 128
+#define FLOWKV_INLINE_RUNS 64 /* plan records flowkv_transfer_inline carries */
 
 typedef struct flowkv_allocator flowkv_allocator; /* opaque, host memory only */
 
@@ -217,6 +218,18 @@ int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst,
                        const flowkv_segment* segs_dev, int64_t n_segs,
                        int64_t total_blocks, const flowkv_launch_config* cfg,
                        void* hip_stream);
+
+/* flowkv_transfer_ex for small plans held in host memory: the records
+   (at most FLOWKV_INLINE_RUNS) are copied into the kernel's arguments at
+   launch, so the plan needs no device buffer and no separate host-to-device
+   copy; segs_host may be reused as soon as the call returns.  Same result as
+   flowkv_transfer_ex with the same plan in device memory.  ECAP when n_segs
+   exceeds FLOWKV_INLINE_RUNS (use flowkv_transfer_ex with a device plan);
+   other arguments and errors as for flowkv_transfer_ex. */
+int flowkv_transfer_inline(const flowkv_pool* src, const flowkv_pool* dst,
+                           const flowkv_segment* segs_host, int64_t n_segs,
+                           int64_t total_blocks, const flowkv_launch_config* cfg,
+                           void* hip_stream);
 
 /* Layer-wise variant (section 4.4 and Table 3: the "FlowKV-Layerwise"
    ablation, which moves the KV cache one layer at a time, as a sender that

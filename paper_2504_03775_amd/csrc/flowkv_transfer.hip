@@ -47,6 +47,9 @@ struct PoolArg {
   int64_t num_blocks;
 };
 
+// Plans of up to kInlineRuns records can travel inside the kernel arguments.
+constexpr int kInlineRuns = FLOWKV_INLINE_RUNS;
+
 struct XferArgs {
   PoolArg src;
   PoolArg dst;
@@ -67,7 +70,9 @@ struct XferArgs {
   uint32_t h_shift;
   int32_t order;            // 1 plan order, 2 blocks scattered, 3 tiles scattered
   int64_t perm_mul;         // multiplier of the scattering permutation
+  flowkv_segment inline_runs[kInlineRuns];  // the plan, when it rides in the arguments
 };
+static_assert(sizeof(XferArgs) <= 4096, "kernel arguments must stay within 4 KiB");
 
 // Pool memory is global memory; naming the address space lets the compiler
 // emit global (not flat) vector loads and stores with a scalar base.
@@ -215,15 +220,31 @@ __device__ __forceinline__ void copy_tile_lanes(const XferArgs& a, char* const* 
   }
 }
 
+// Record i of the plan: from device memory (read through the constant
+// address space) or from the kernel arguments.  Both stay on the scalar unit.
+template <bool kInline>
+__device__ __forceinline__ int32_t run_first(const XferArgs& a, const cseg* segs, int32_t i) {
+  if constexpr (kInline) return a.inline_runs[i].first;
+  else return segs[i].first;
+}
+
+template <bool kInline>
+__device__ __forceinline__ flowkv_segment run_at(const XferArgs& a, const cseg* segs, int32_t i) {
+  if constexpr (kInline) return a.inline_runs[i];
+  else return load_seg(segs + i);
+}
+
 // Index of the last run whose first block is <= g, by galloping from run s
 // (backward or forward) to a bracket [lo, hi) with first[lo] <= g < first[hi]
 // and bisecting it.  Always returns an index in [0, n).
-__device__ __forceinline__ int32_t find_run(const cseg* segs, int32_t n, int64_t g, int32_t s) {
+template <bool kInline>
+__device__ __forceinline__ int32_t find_run(const XferArgs& a, const cseg* segs, int32_t n,
+                                            int64_t g, int32_t s) {
   int32_t lo, hi, step = 1;
-  if (segs[s].first > g) {
+  if (run_first<kInline>(a, segs, s) > g) {
     hi = s;
     lo = s - 1;
-    while (lo > 0 && segs[lo].first > g) {
+    while (lo > 0 && run_first<kInline>(a, segs, lo) > g) {
       hi = lo;
       step <<= 1;
       lo = hi - step > 0 ? hi - step : 0;
@@ -232,7 +253,7 @@ __device__ __forceinline__ int32_t find_run(const cseg* segs, int32_t n, int64_t
   } else {
     lo = s;
     hi = s + 1;
-    while (hi < n && segs[hi].first <= g) {
+    while (hi < n && run_first<kInline>(a, segs, hi) <= g) {
       lo = hi;
       step <<= 1;
       hi = lo + step < n ? lo + step : n;
@@ -240,7 +261,7 @@ __device__ __forceinline__ int32_t find_run(const cseg* segs, int32_t n, int64_t
   }
   while (hi - lo > 1) {
     const int32_t mid = (lo + hi) >> 1;
-    if (segs[mid].first <= g) lo = mid;
+    if (run_first<kInline>(a, segs, mid) <= g) lo = mid;
     else hi = mid;
   }
   return lo;
@@ -252,7 +273,7 @@ __device__ __forceinline__ int32_t guess_run(const XferArgs& a, int64_t g) {
   return int32_t(s < a.n_segs ? s : a.n_segs - 1);
 }
 
-template <bool kSrcLM, bool kDstLM, int kU, int kCache, bool kUniform>
+template <bool kSrcLM, bool kDstLM, int kU, int kCache, bool kUniform, bool kInline>
 __global__ __launch_bounds__(1024) void kv_segment_copy(const XferArgs a) {
   __shared__ char* s_src[kUniform ? 1 : FLOWKV_MAX_LAYERS];
   __shared__ char* s_dst[kUniform ? 1 : FLOWKV_MAX_LAYERS];
@@ -295,8 +316,8 @@ __global__ __launch_bounds__(1024) void kv_segment_copy(const XferArgs a) {
       t = int32_t(v - g * a.tiles_per_block);
     }
     if (s < 0 || g < seg.first || g - seg.first >= int64_t(seg.n_blocks)) {
-      s = find_run(segs, a.n_segs, g, (s < 0 || a.order != 1) ? guess_run(a, g) : s);
-      seg = load_seg(segs + s);
+      s = find_run<kInline>(a, segs, a.n_segs, g, (s < 0 || a.order != 1) ? guess_run(a, g) : s);
+      seg = run_at<kInline>(a, segs, s);
     }
     const int64_t off = g - seg.first;
     const int64_t sb = int64_t(seg.src_block) + off;
@@ -321,36 +342,42 @@ __global__ __launch_bounds__(1024) void kv_segment_copy(const XferArgs a) {
 
 using KernelFn = void (*)(XferArgs);
 
-template <bool S, bool D, int U, int C>
+template <bool S, bool D, int U, int C, bool I>
 KernelFn pick_path(bool uniform) {
-  return uniform ? kv_segment_copy<S, D, U, C, true> : kv_segment_copy<S, D, U, C, false>;
+  return uniform ? kv_segment_copy<S, D, U, C, true, I> : kv_segment_copy<S, D, U, C, false, I>;
 }
 
-template <bool S, bool D, int U>
+template <bool S, bool D, int U, bool I>
 KernelFn pick_cache(int cache, bool uniform) {
   switch (cache) {
-    case 0: return pick_path<S, D, U, 0>(uniform);
-    case 1: return pick_path<S, D, U, 1>(uniform);
-    case 2: return pick_path<S, D, U, 2>(uniform);
-    default: return pick_path<S, D, U, 3>(uniform);
+    case 0: return pick_path<S, D, U, 0, I>(uniform);
+    case 1: return pick_path<S, D, U, 1, I>(uniform);
+    case 2: return pick_path<S, D, U, 2, I>(uniform);
+    default: return pick_path<S, D, U, 3, I>(uniform);
   }
 }
 
-template <bool S, bool D>
+template <bool S, bool D, bool I>
 KernelFn pick_unroll(int unroll, int cache, bool uniform) {
   switch (unroll) {
-    case 2: return pick_cache<S, D, 2>(cache, uniform);
-    case 4: return pick_cache<S, D, 4>(cache, uniform);
-    case 8: return pick_cache<S, D, 8>(cache, uniform);
-    default: return pick_cache<S, D, 16>(cache, uniform);
+    case 2: return pick_cache<S, D, 2, I>(cache, uniform);
+    case 4: return pick_cache<S, D, 4, I>(cache, uniform);
+    case 8: return pick_cache<S, D, 8, I>(cache, uniform);
+    default: return pick_cache<S, D, 16, I>(cache, uniform);
   }
 }
 
-KernelFn pick_kernel(bool src_lm, bool dst_lm, int unroll, int cache, bool uniform) {
-  if (src_lm && dst_lm) return pick_unroll<true, true>(unroll, cache, uniform);
-  if (src_lm) return pick_unroll<true, false>(unroll, cache, uniform);
-  if (dst_lm) return pick_unroll<false, true>(unroll, cache, uniform);
-  return pick_unroll<false, false>(unroll, cache, uniform);
+template <bool I>
+KernelFn pick_layouts(bool src_lm, bool dst_lm, int unroll, int cache, bool uniform) {
+  if (src_lm && dst_lm) return pick_unroll<true, true, I>(unroll, cache, uniform);
+  if (src_lm) return pick_unroll<true, false, I>(unroll, cache, uniform);
+  if (dst_lm) return pick_unroll<false, true, I>(unroll, cache, uniform);
+  return pick_unroll<false, false, I>(unroll, cache, uniform);
+}
+
+KernelFn pick_kernel(bool src_lm, bool dst_lm, int unroll, int cache, bool uniform, bool inl) {
+  return inl ? pick_layouts<true>(src_lm, dst_lm, unroll, cache, uniform)
+             : pick_layouts<false>(src_lm, dst_lm, unroll, cache, uniform);
 }
 
 // Library defaults, from interleaved launch-shape comparisons over the five
@@ -431,9 +458,10 @@ bool overlaps(const Range& x, const Range& y) { return x.lo < y.hi && y.lo < x.h
 namespace {
 
 int launch_transfer(const flowkv_pool* src, const flowkv_pool* dst,
-                    const flowkv_segment* segs_dev, int64_t n_segs, int64_t total_blocks,
-                    int32_t layer_begin, int32_t layer_count, bool whole,
-                    const flowkv_launch_config* cfg, void* hip_stream) {
+                    const flowkv_segment* segs_dev, const flowkv_segment* segs_host,
+                    int64_t n_segs, int64_t total_blocks, int32_t layer_begin,
+                    int32_t layer_count, bool whole, const flowkv_launch_config* cfg,
+                    void* hip_stream) {
   Range rs[FLOWKV_MAX_LAYERS], rd[FLOWKV_MAX_LAYERS];
   int ns = 0, nd = 0;
   int rc = pool_ranges(src, "sender", rs, &ns);
@@ -479,9 +507,13 @@ int launch_transfer(const flowkv_pool* src, const flowkv_pool* dst,
     return fail(FLOWKV_EINVAL, "unroll %d: need 2, 4, 8 or 16", unroll);
   if (cache < 1 || cache > 4) return fail(FLOWKV_EINVAL, "cache %d: need 1..4", cache);
   if (grid < 0) return fail(FLOWKV_EINVAL, "negative grid %d", grid);
+  const bool inl = segs_host != nullptr;
+  if (inl && n_segs > kInlineRuns)
+    return fail(FLOWKV_ECAP, "%lld runs, at most %d travel in the kernel arguments",
+                (long long)n_segs, kInlineRuns);
   if (n_segs == 0 || total_blocks == 0 || layer_count == 0) return ok();
-  if (!segs_dev) return fail(FLOWKV_EINVAL, "NULL segment list");
-  if (reinterpret_cast<uintptr_t>(segs_dev) % 16)
+  if (!inl && !segs_dev) return fail(FLOWKV_EINVAL, "NULL segment list");
+  if (!inl && reinterpret_cast<uintptr_t>(segs_dev) % 16)
     return fail(FLOWKV_EINVAL, "segment list not 16-byte aligned");
 
   XferArgs a{};
@@ -489,7 +521,9 @@ int launch_transfer(const flowkv_pool* src, const flowkv_pool* dst,
   for (int i = 0; i < nd; ++i) a.dst.base[i] = static_cast<char*>(dst->layer_base[i]);
   a.src.num_blocks = src->num_blocks;
   a.dst.num_blocks = dst->num_blocks;
-  a.segs = segs_dev;
+  a.segs = inl ? nullptr : segs_dev;
+  if (inl)
+    for (int64_t i = 0; i < n_segs; ++i) a.inline_runs[i] = segs_host[i];
   a.n_segs = int32_t(n_segs);
   a.num_layers = src->num_layers;
   a.chunk_bytes = src->chunk_bytes;
@@ -535,7 +569,8 @@ int launch_transfer(const flowkv_pool* src, const flowkv_pool* dst,
   launch = std::min<int64_t>(launch, INT32_MAX);
 
   KernelFn fn = pick_kernel(src->layout == FLOWKV_LAYOUT_LAYER_MAJOR,
-                            dst->layout == FLOWKV_LAYOUT_LAYER_MAJOR, unroll, cache - 1, uniform);
+                            dst->layout == FLOWKV_LAYOUT_LAYER_MAJOR, unroll, cache - 1, uniform,
+                            inl);
   void* args[] = {&a};
   hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(launch)),
                                  dim3(unsigned(threads)), args, 0,
@@ -551,7 +586,18 @@ extern "C" int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst
                                   const flowkv_segment* segs_dev, int64_t n_segs,
                                   int64_t total_blocks, const flowkv_launch_config* cfg,
                                   void* hip_stream) {
-  return launch_transfer(src, dst, segs_dev, n_segs, total_blocks, 0, 0, true, cfg, hip_stream);
+  return launch_transfer(src, dst, segs_dev, nullptr, n_segs, total_blocks, 0, 0, true, cfg,
+                         hip_stream);
+}
+
+extern "C" int flowkv_transfer_inline(const flowkv_pool* src, const flowkv_pool* dst,
+                                      const flowkv_segment* segs_host, int64_t n_segs,
+                                      int64_t total_blocks, const flowkv_launch_config* cfg,
+                                      void* hip_stream) {
+  if (n_segs > 0 && !segs_host) return fail(FLOWKV_EINVAL, "NULL segment list");
+  static const flowkv_segment none{};
+  return launch_transfer(src, dst, nullptr, segs_host ? segs_host : &none, n_segs, total_blocks,
+                         0, 0, true, cfg, hip_stream);
 }
 
 extern "C" int flowkv_transfer_layers(const flowkv_pool* src, const flowkv_pool* dst,
@@ -559,8 +605,8 @@ extern "C" int flowkv_transfer_layers(const flowkv_pool* src, const flowkv_pool*
                                       int64_t total_blocks, int32_t layer_begin,
                                       int32_t layer_count, const flowkv_launch_config* cfg,
                                       void* hip_stream) {
-  return launch_transfer(src, dst, segs_dev, n_segs, total_blocks, layer_begin, layer_count,
-                         false, cfg, hip_stream);
+  return launch_transfer(src, dst, segs_dev, nullptr, n_segs, total_blocks, layer_begin,
+                         layer_count, false, cfg, hip_stream);
 }
 
 extern "C" int flowkv_transfer(const flowkv_pool* src, const flowkv_pool* dst,

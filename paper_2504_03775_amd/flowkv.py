@@ -23,6 +23,7 @@ OK, EINVAL, ENOSPC, ERANGE, EDUP, ECAP, EHIP = 0, -1, -2, -3, -4, -5, -6
 POLICY_SEGMENT, POLICY_FIFO_SORTED, POLICY_FIFO_SHUFFLED = 0, 1, 2
 LAYOUT_LAYER_MAJOR, LAYOUT_BLOCK_MAJOR = 0, 1
 MAX_LAYERS = 128
+INLINE_RUNS = 64  # plan records flowkv_transfer_inline carries in the kernel arguments
 
 SEGMENT_DTYPE = np.dtype([("src_block", "<i4"), ("dst_block", "<i4"),
                           ("n_blocks", "<i4"), ("first", "<i4")])
@@ -80,6 +81,9 @@ SIGNATURES = {
     "flowkv_transfer_ex": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_int64,
                                           ctypes.c_int64, ctypes.POINTER(flowkv_launch_config),
                                           ctypes.c_void_p]),
+    "flowkv_transfer_inline": (ctypes.c_int, [_POOLP, _POOLP, _SEGP, ctypes.c_int64,
+                                              ctypes.c_int64, ctypes.POINTER(flowkv_launch_config),
+                                              ctypes.c_void_p]),
     "flowkv_transfer_layers": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_int64,
                                               ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                               ctypes.POINTER(flowkv_launch_config),
@@ -307,6 +311,19 @@ def flowkv_transfer_ex(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_bl
                                    n_segs, total_blocks, ctypes.byref(cfg),
                                    ctypes.c_void_p(_stream_handle(stream))),
            "flowkv_transfer_ex")
+
+
+def flowkv_transfer_inline(src: KVPool, dst: KVPool, segs: np.ndarray, total_blocks: int,
+                           threads: int = 0, unroll: int = 0, grid: int = 0, cache: int = 0,
+                           order: int = 0, stream=None) -> None:
+    """Enqueue the one-launch copy with a host plan (SEGMENT_DTYPE array of at
+    most INLINE_RUNS records) carried in the kernel arguments."""
+    segs = np.ascontiguousarray(segs, dtype=SEGMENT_DTYPE)
+    cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
+    _check(_lib.flowkv_transfer_inline(ctypes.byref(src.desc), ctypes.byref(dst.desc),
+                                       segs.ctypes.data_as(_SEGP), len(segs), total_blocks,
+                                       ctypes.byref(cfg), ctypes.c_void_p(_stream_handle(stream))),
+           "flowkv_transfer_inline")
 
 
 def flowkv_transfer_layers(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_blocks: int,

@@ -258,6 +258,17 @@ def test_transfer_rejects_bad_pools_without_touching_the_device():
     for l0, lc in ((-1, 1), (0, 3), (2, 1), (1, 2), (0, -1)):
         assert xfer_layers(l0, lc) == fk.EINVAL, (l0, lc)
     assert xfer_layers(1, 0) == fk.OK  # nothing to move: no launch
+    # plans carried in the kernel arguments: at most INLINE_RUNS records
+    big = np.zeros(fk.INLINE_RUNS + 1, dtype=fk.SEGMENT_DTYPE)
+    rc = fk.lib().flowkv_transfer_inline(ctypes.byref(good_src), ctypes.byref(good_dst),
+                                         big.ctypes.data_as(fk._SEGP), len(big), 1, None, None)
+    assert rc == fk.ECAP
+    rc = fk.lib().flowkv_transfer_inline(ctypes.byref(good_src), ctypes.byref(good_dst),
+                                         None, 1, 1, None, None)
+    assert rc == fk.EINVAL
+    rc = fk.lib().flowkv_transfer_inline(ctypes.byref(good_src), ctypes.byref(good_dst),
+                                         None, 0, 0, None, None)
+    assert rc == fk.OK
     assert xfer(good_src, good_dst, segs=8) == fk.EINVAL  # misaligned plan
     assert xfer(good_src, good_dst, segs=0) == fk.EINVAL  # NULL plan
     assert xfer(good_src, good_dst, n_segs=-1) == fk.EINVAL

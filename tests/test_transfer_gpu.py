@@ -247,3 +247,44 @@ def test_one_launch_per_layer_equals_one_launch(sl, dl):
         fk.flowkv_transfer_layers(src, d2, dev, len(segs), 5, l, 1)
     torch.cuda.synchronize()
     assert host_equal(download_all(d1), download_all(d2))
+
+
+# ---- plans carried in the kernel arguments -----------------------------------
+
+@pytest.mark.parametrize("seed", range(12))
+def test_inline_plans_against_oracle(seed):
+    geom, Bs, Bd, tables = random_case(2000 + seed)
+    sl, dl = LAYOUT_PAIRS[seed % 4]
+    cfg = CONFIGS[seed % len(CONFIGS)]
+    segs, S, D = plan_tables(tables, Bs, Bd)
+    if len(segs) > fk.INLINE_RUNS:
+        pytest.skip("plan longer than the inline limit")
+    say(f"inline seed={seed} runs={len(segs)} n={len(S)} {NAMES[sl]}->{NAMES[dl]} cfg={cfg}")
+    src = device_pool(geom, sl, Bs, seed)
+    dst = device_pool(geom, dl, Bd, seed + 1)
+    h_src, h_dst = download_all(src), download_all(dst)
+    fk.flowkv_transfer_inline(src, dst, segs, fk.plan_total_blocks(segs), **cfg)
+    torch.cuda.synchronize()
+    oracle.transfer_batch_fast(h_src, h_dst, [(s_, d_) for s_, d_ in tables])
+    assert host_equal(download_all(dst), h_dst)
+
+
+def test_inline_plan_at_the_limit_equals_device_plan():
+    """64 one-block runs (the inline limit) at the 8B geometry: the inline and
+    the device-memory plan give the same receiver pool, and match the oracle."""
+    geom = LLAMA3_8B
+    src = device_pool(geom, BM, 130, 0)
+    d1 = device_pool(geom, LM, 130, 1)
+    d2 = device_pool(geom, LM, 130, 1)
+    h_src, h_dst = download_all(src), download_all(d1)
+    S = 2 * np.arange(64, dtype=np.int32)
+    D = 2 * np.arange(64, dtype=np.int32) + 1
+    segs = fk.flowkv_plan(S, D, 130, 130)
+    assert len(segs) == fk.INLINE_RUNS
+    fk.flowkv_transfer_inline(src, d1, segs, 64)
+    fk.flowkv_transfer(src, d2, fk.segments_to_device(segs, src.device), len(segs), 64)
+    torch.cuda.synchronize()
+    oracle.transfer_fast(h_src, h_dst, S, D)
+    got = download_all(d1)
+    assert host_equal(got, h_dst)
+    assert host_equal(got, download_all(d2))
