@@ -1,0 +1,145 @@
+"""Pins for the decode-attention oracle (``oracle.attention``), CPU only.
+
+The oracle gathers K and V slot by slot with the pool's own address formulas
+and runs softmax attention per query head.  These tests build pools through
+numpy's shaped views of the Eq. 5 layouts and check the oracle against
+closed forms and against a separate dense computation (np.repeat for the
+grouped heads, scipy's logsumexp for the normaliser, einsum for the products).
+"""
+
+import numpy as np
+import pytest
+from scipy.special import logsumexp
+
+from oracle import BLOCK_MAJOR, LAYER_MAJOR, HostPool
+from oracle.attention import decode_attention
+
+LAYOUTS = [LAYER_MAJOR, BLOCK_MAJOR]
+
+
+def to_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float values to bfloat16 (nearest-even); returns uint16 patterns."""
+    f = np.asarray(x, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return u.astype(np.uint16)
+
+
+def from_bf16(u: np.ndarray) -> np.ndarray:
+    return (u.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def build_pool(layout, L, B, bs, hkv, dh, layer, tables, kv_tokens):
+    """Pool whose blocks hold, for layer `layer`, the bf16 patterns
+    kv_tokens[r][kv, t, g, d] of each request's token t at its slot."""
+    pool = HostPool.zeros(layout, L, B, bs, hkv * dh * 2)
+    if layout == BLOCK_MAJOR:
+        v = pool.buffers[0].view(np.uint16).reshape(B, L, 2, bs, hkv, dh)
+    else:
+        v = [b.view(np.uint16).reshape(2, B, bs, hkv, dh) for b in pool.buffers]
+    for table, kvt in zip(tables, kv_tokens):
+        for t in range(kvt.shape[1]):
+            b, s = table[t // bs], t % bs
+            for kv in (0, 1):
+                if layout == BLOCK_MAJOR:
+                    v[b, layer, kv, s] = kvt[kv, t]
+                else:
+                    v[layer][kv, b, s] = kvt[kv, t]
+    return pool
+
+
+def dense_reference(q, kv_f64, hq, hkv, scale):
+    """Softmax attention on contiguous (2, T, hkv, dh) K/V of one request."""
+    K = np.repeat(kv_f64[0], hq // hkv, axis=1)   # (T, hq, dh)
+    V = np.repeat(kv_f64[1], hq // hkv, axis=1)
+    s = scale * np.einsum("hd,thd->ht", q, K)
+    p = np.exp(s - logsumexp(s, axis=1, keepdims=True))
+    return np.einsum("ht,thd->hd", p, V)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_matches_dense_attention(layout):
+    rng = np.random.default_rng(1)
+    L, B, bs, hkv, dh, hq = 3, 12, 4, 2, 16, 8
+    layer = 2
+    lens = [1, 7, 13]
+    # requests' blocks are distinct
+    tables = []
+    perm = rng.permutation(B)
+    pos = 0
+    for T in lens:
+        nb = -(-T // bs)
+        tables.append(perm[pos:pos + nb])
+        pos += nb
+    kv_bits = [to_bf16(rng.standard_normal((2, T, hkv, dh))) for T in lens]
+    pool = build_pool(layout, L, B, bs, hkv, dh, layer, tables, kv_bits)
+    q = from_bf16(to_bf16(rng.standard_normal((len(lens), hq, dh))))
+    scale = 1 / np.sqrt(dh)
+    got = decode_attention(pool, q, tables, lens, layer, hkv, dh, scale)
+    for r, T in enumerate(lens):
+        want = dense_reference(q[r], from_bf16(kv_bits[r]), hq, hkv, scale)
+        np.testing.assert_allclose(got[r], want, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_closed_forms(layout):
+    rng = np.random.default_rng(2)
+    L, B, bs, hkv, dh, hq = 2, 6, 2, 1, 8, 2
+    scale = 0.5
+    # one token: the output is that token's V exactly
+    kv = to_bf16(rng.standard_normal((2, 1, hkv, dh)))
+    pool = build_pool(layout, L, B, bs, hkv, dh, 1, [[4]], [kv])
+    q = rng.standard_normal((1, hq, dh))
+    got = decode_attention(pool, q, [[4]], [1], 1, hkv, dh, scale)
+    assert np.array_equal(got[0, 0], from_bf16(kv[1, 0, 0]))
+    # a zero query scores every key equally: the output is the mean of V
+    T = 5
+    kv = to_bf16(rng.standard_normal((2, T, hkv, dh)))
+    pool = build_pool(layout, L, B, bs, hkv, dh, 0, [[3, 0, 5]], [kv])
+    got = decode_attention(pool, np.zeros((1, hq, dh)), [[3, 0, 5]], [T], 0, hkv, dh, scale)
+    np.testing.assert_allclose(got[0, 1], from_bf16(kv[1, :, 0]).mean(axis=0), rtol=1e-12)
+    # a query that singles out key j returns V[j] (up to exp(-big) weights)
+    keys = np.zeros((T, hkv, dh))
+    for t in range(T):
+        keys[t, 0, t] = 1.0
+    kv = np.stack([to_bf16(keys), to_bf16(rng.standard_normal((T, hkv, dh)))])
+    pool = build_pool(layout, L, B, bs, hkv, dh, 0, [[3, 0, 5]], [kv])
+    j = 3
+    qj = np.zeros((1, hq, dh))
+    qj[0, :, j] = 200.0
+    got = decode_attention(pool, qj, [[3, 0, 5]], [T], 0, hkv, dh, scale)
+    np.testing.assert_allclose(got[0, 0], from_bf16(kv[1, j, 0]), rtol=1e-12, atol=1e-30)
+    # scores far beyond exp's range (s = 1000) still give a finite, exact
+    # answer: the normaliser is taken relative to the largest score
+    qj[0, :, j] = 2000.0
+    got = decode_attention(pool, qj, [[3, 0, 5]], [T], 0, hkv, dh, scale)
+    assert np.all(np.isfinite(got))
+    np.testing.assert_allclose(got[0, 0], from_bf16(kv[1, j, 0]), rtol=1e-12, atol=1e-30)
+
+
+def test_block_relabelling_does_not_change_the_result():
+    rng = np.random.default_rng(3)
+    L, B, bs, hkv, dh, hq = 2, 10, 4, 2, 8, 4
+    T = 15
+    kv = to_bf16(rng.standard_normal((2, T, hkv, dh)))
+    q = rng.standard_normal((1, hq, dh))
+    outs = []
+    for seed in range(3):
+        table = np.random.default_rng(seed).permutation(B)[:4]
+        pool = build_pool(BLOCK_MAJOR, L, B, bs, hkv, dh, 1, [table], [kv])
+        outs.append(decode_attention(pool, q, [table], [T], 1, hkv, dh, 0.3))
+    for o in outs[1:]:
+        assert np.array_equal(o, outs[0])
+
+
+def test_rejects_bad_inputs():
+    pool = HostPool.zeros(BLOCK_MAJOR, 1, 4, 2, 16)
+    with pytest.raises(ValueError):
+        decode_attention(pool, np.zeros((1, 2, 8)), [[0]], [1], 0, 2, 8, 1.0)  # slot size
+    pool = HostPool.zeros(BLOCK_MAJOR, 1, 4, 2, 2 * 8 * 2)
+    with pytest.raises(ValueError):
+        decode_attention(pool, np.zeros((1, 3, 8)), [[0]], [1], 0, 2, 8, 1.0)  # 3 % 2
+    with pytest.raises(ValueError):
+        decode_attention(pool, np.zeros((1, 2, 8)), [[0]], [3], 0, 2, 8, 1.0)  # T > blocks
+    with pytest.raises(ValueError):
+        decode_attention(pool, np.zeros((1, 2, 8)), [[0]], [0], 0, 2, 8, 1.0)  # T = 0
