@@ -68,6 +68,9 @@ WORKLOADS = {
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--op", choices=["transfer", "attention"], default="transfer",
+                    help="transfer: the KV transfer hot path (default); attention: one decode "
+                         "step of paged attention over the receiver pool of the batch workload")
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="8b")
@@ -112,12 +115,89 @@ def traffic_from_profile():
     return float(t.group(1)) if t else None
 
 
+def bench_attention(args):
+    """Decode attention (one layer, one new token per request) over the
+    receiver pool of the 32-request batch workload: 32 query heads on 8 KV
+    heads, head_dim 128, block 16, 2,000-20,000 tokens per request."""
+    import numpy as np
+    import torch
+
+    from paper_2504_03775_amd import flowkv as fk
+    from workloads import make_device_pool, recipes
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    layout = fk.LAYOUT_BLOCK_MAJOR if args.layout == "block" else fk.LAYOUT_LAYER_MAJOR
+    wl = recipes.batch32(lambda P, pol, seed: fk.Allocator(P, pol, seed), "segment")
+    geom = wl.geom
+    q_heads = 32
+    pool = fk.KVPool(layout, make_device_pool(geom, layout, wl.dst_pool_blocks, dev, seed=1))
+    lens = np.asarray(wl.tokens, dtype=np.int32)
+    max_blocks = max(len(d) for _, d in wl.tables)
+    tab = np.full((len(lens), max_blocks), -1, dtype=np.int32)
+    for r, (_, d) in enumerate(wl.tables):
+        tab[r, :len(d)] = d
+    tab_d = torch.as_tensor(tab, device=dev)
+    lens_d = torch.as_tensor(lens, device=dev)
+    q = torch.randn((len(lens), q_heads, geom.head_dim), device=dev).to(torch.bfloat16)
+    out = torch.empty((len(lens), q_heads, geom.head_dim), dtype=torch.float32, device=dev)
+    max_seq = int(lens.max())
+    ws = torch.empty(fk.flowkv_decode_attention_workspace(len(lens), q_heads, geom.head_dim,
+                                                          max_seq), dtype=torch.uint8, device=dev)
+    scale = 1.0 / geom.head_dim ** 0.5
+    layer = geom.num_layers // 2
+
+    def step():
+        fk.flowkv_decode_attention(pool, layer, q, tab_d, lens_d, max_seq, scale, out, ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    gc.collect()
+    gc.disable()
+    t0 = time.perf_counter()
+    for e in evs:
+        e[0].record()
+        step()
+        e[1].record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    gc.enable()
+    ms = statistics.fmean(a.elapsed_time(b) for a, b in evs)
+    kv_bytes = int(lens.sum()) * 2 * geom.kv_heads * geom.head_dim * 2
+    splits = -(-max_seq // 256)
+    ws_bytes = 2 * len(lens) * q_heads * splits * (geom.head_dim + 2) * 4
+    algo = kv_bytes + q.numel() * 2 + out.numel() * 4 + ws_bytes + tab.nbytes
+    achieved = algo / (ms * 1e-3) / 1e9
+    line = {
+        "metric": "decode attention HBM GB/s (one layer, one token per request)",
+        "value": round(achieved, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "llama3-8b-decode-attention-batch-32-requests-2k-20k",
+                   "requests": len(lens), "tokens": int(lens.sum()), "q_heads": q_heads,
+                   "kv_heads": geom.kv_heads, "head_dim": geom.head_dim,
+                   "block_size": geom.block_size, "kv_dtype": "bf16",
+                   "layout": f"{args.layout}-major", "layer": layer},
+        "kernel_ms_avg": round(ms, 4),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None},
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the transfer "
               "path in this build is single-device.", file=sys.stderr)
         sys.exit(2)
+    if args.op == "attention":
+        bench_attention(args)
+        return
 
     import numpy as np
     import torch

@@ -244,6 +244,43 @@ int flowkv_transfer_layers(const flowkv_pool* src, const flowkv_pool* dst,
                            int64_t total_blocks, int32_t layer_begin, int32_t layer_count,
                            const flowkv_launch_config* cfg, void* hip_stream);
 
+/* ---- decode attention over a pool (section 3.3: the PagedAttention kernel
+        adapted to the restructured layout; the decode step of Eq. 2) -------- */
+
+#define FLOWKV_ATTN_DEFAULT_SPLIT 256 /* tokens per pass-1 workgroup */
+#define FLOWKV_ATTN_MAX_SPLIT 1024
+
+/* Workspace bytes flowkv_decode_attention needs for n_req requests of at most
+   max_seq_len tokens: n_req x q_heads x ceil(max_seq_len / split_tokens) x
+   (head_dim + 2) floats.  split_tokens 0 = FLOWKV_ATTN_DEFAULT_SPLIT. */
+int flowkv_decode_attention_workspace(int32_t n_req, int32_t q_heads, int32_t head_dim,
+                                      int32_t max_seq_len, int32_t split_tokens,
+                                      int64_t* bytes);
+
+/* One decode step of attention for n_req requests, layer `layer` of a bf16
+   pool (either layout; the pool's chunk_bytes must be block_size x kv_heads x
+   head_dim x 2).  For request r and query head h (KV head g = h / (q_heads /
+   kv_heads)), with T = seq_lens[r] tokens in blocks block_tables[r][0..]:
+       out[r][h] = sum_t softmax_t(scale * q[r][h] . K[t][g]) * V[t][g]
+   Token t lives in block block_tables[r * max_blocks + t / block_size], slot
+   t % block_size.  Device inputs: q (n_req, q_heads, head_dim) bf16, 16-byte
+   aligned; block_tables (n_req, max_blocks) int32; seq_lens (n_req) int32.
+   Output: out (n_req, q_heads, head_dim) float32.  workspace: device memory
+   of at least flowkv_decode_attention_workspace(...) bytes, owned by the
+   caller, busy until the stream passes the call.  Tokens beyond
+   max_blocks x block_size or beyond max_seq_len are not read; a block ID
+   outside the pool contributes nothing; a request with no tokens gets zeros.
+   head_dim 64 or 128; q_heads / kv_heads in {1, 2, 4, 8}; split_tokens 0 =
+   default, else 1..FLOWKV_ATTN_MAX_SPLIT.  Two launches on hip_stream.
+   EINVAL for bad shapes or pointers, ECAP for a short workspace. */
+int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer, const void* q_dev,
+                            int32_t n_req, int32_t q_heads, int32_t kv_heads,
+                            int32_t head_dim, const int32_t* block_tables_dev,
+                            int32_t max_blocks, const int32_t* seq_lens_dev,
+                            int32_t max_seq_len, float scale, int32_t split_tokens,
+                            float* out_dev, void* workspace_dev, int64_t workspace_bytes,
+                            void* hip_stream);
+
 /* ---- diagnostics ------------------------------------------------------------ */
 
 /* Static name of a status code. */

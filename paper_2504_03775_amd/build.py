@@ -20,7 +20,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libflowkv.so")
 
 HOST_SOURCES = ["flowkv_status.cpp", "flowkv_alloc.cpp", "flowkv_plan.cpp"]
-HIP_SOURCES = ["flowkv_transfer.hip"]
+HIP_SOURCES = ["flowkv_transfer.hip", "flowkv_attention.hip"]
 
 ARCH = "gfx950"
 # packed-fp32 instructions are disabled for every HIP translation unit

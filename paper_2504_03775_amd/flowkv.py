@@ -88,6 +88,15 @@ SIGNATURES = {
                                               ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                               ctypes.POINTER(flowkv_launch_config),
                                               ctypes.c_void_p]),
+    "flowkv_decode_attention_workspace": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32,
+                                                         ctypes.c_int32, ctypes.c_int32,
+                                                         ctypes.c_int32, _I64P]),
+    "flowkv_decode_attention": (ctypes.c_int, [_POOLP, ctypes.c_int32, ctypes.c_void_p,
+                                               ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                               ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                                               ctypes.c_void_p, ctypes.c_int32, ctypes.c_float,
+                                               ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                               ctypes.c_int64, ctypes.c_void_p]),
     "flowkv_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "flowkv_last_error": (ctypes.c_char_p, []),
 }
@@ -336,6 +345,39 @@ def flowkv_transfer_layers(src: KVPool, dst: KVPool, segs_dev, n_segs: int, tota
                                        n_segs, total_blocks, layer_begin, layer_count,
                                        ctypes.byref(cfg), ctypes.c_void_p(_stream_handle(stream))),
            "flowkv_transfer_layers")
+
+
+def flowkv_decode_attention_workspace(n_req: int, q_heads: int, head_dim: int,
+                                      max_seq_len: int, split_tokens: int = 0) -> int:
+    b = ctypes.c_int64()
+    _check(_lib.flowkv_decode_attention_workspace(n_req, q_heads, head_dim, max_seq_len,
+                                                  split_tokens, ctypes.byref(b)),
+           "flowkv_decode_attention_workspace")
+    return b.value
+
+
+def flowkv_decode_attention(pool: KVPool, layer: int, q, block_tables, seq_lens,
+                            max_seq_len: int, scale: float, out, workspace,
+                            split_tokens: int = 0, stream=None) -> None:
+    """Decode attention of layer `layer` over `pool` (torch device tensors:
+    q (n, Hq, Dh) bf16, block_tables (n, max_blocks) int32, seq_lens (n,)
+    int32, out (n, Hq, Dh) float32, workspace uint8)."""
+    import torch
+
+    n, hq, dh = q.shape
+    for t, dt in ((q, torch.bfloat16), (block_tables, torch.int32), (seq_lens, torch.int32),
+                  (out, torch.float32)):
+        if t.dtype != dt or not t.is_contiguous() or t.device != pool.device:
+            raise ValueError("attention tensors: wrong dtype, layout or device")
+    if tuple(out.shape) != (n, hq, dh) or block_tables.shape[0] != n or seq_lens.shape[0] != n:
+        raise ValueError("attention tensors: shapes disagree")
+    _check(_lib.flowkv_decode_attention(
+        ctypes.byref(pool.desc), layer, ctypes.c_void_p(q.data_ptr()), n, hq, pool.kv_heads, dh,
+        ctypes.c_void_p(block_tables.data_ptr()), block_tables.shape[1],
+        ctypes.c_void_p(seq_lens.data_ptr()), max_seq_len, scale, split_tokens,
+        ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(workspace.data_ptr()),
+        workspace.numel() * workspace.element_size(), ctypes.c_void_p(_stream_handle(stream))),
+        "flowkv_decode_attention")
 
 
 def segments_to_device(segs: np.ndarray, device, stream=None):

@@ -1,0 +1,158 @@
+"""GPU parity of paged decode attention against the float64 oracle.
+
+Tolerance, from the arithmetic: K, V and q are bfloat16 (exact in float32);
+scores are float32 dot products of head_dim terms (relative error a few
+1e-6), softmax weights use float32 exp2 (about 1 ulp), and the weighted sums
+of V accumulate at most ~1,300 float32 terms per lane group before the
+merges (relative error below 1e-4 of the weighted |V| mean).  So every output
+element must satisfy |out - oracle| <= 2e-4 * max|V| + 1e-6.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.attention import decode_attention
+from paper_2504_03775_amd import flowkv as fk
+from workloads import Geometry, make_device_pool
+from tests.gpu_helpers import BM, LM, download_blocks
+
+pytestmark = pytest.mark.gpu
+NAMES = {LM: "layer", BM: "block"}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def bf16_to_f64(t: torch.Tensor) -> np.ndarray:
+    u = t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16).astype(np.uint32)
+    return (u << 16).view(np.float32).astype(np.float64)
+
+
+def run_case(geom: Geometry, layout, pool_blocks, lens, q_heads, seed, split=0, layer=None,
+             max_seq=None, check=True):
+    g = np.random.default_rng(seed)
+    layer = int(g.integers(geom.num_layers)) if layer is None else layer
+    pool = fk.KVPool(layout, make_device_pool(geom, layout, pool_blocks, "cuda", seed))
+    bs = geom.block_size
+    nblk = [max(1, -(-T // bs)) for T in lens]
+    perm = g.permutation(pool_blocks)
+    assert sum(nblk) <= pool_blocks
+    tables, pos = [], 0
+    for k in nblk:
+        tables.append(perm[pos:pos + k].astype(np.int32))
+        pos += k
+    max_blocks = max(nblk)
+    tab = np.full((len(lens), max_blocks), -1, dtype=np.int32)
+    for r, t in enumerate(tables):
+        tab[r, :len(t)] = t
+    n = len(lens)
+    q = torch.randn((n, q_heads, geom.head_dim), generator=torch.Generator("cuda").manual_seed(
+        seed + 7), device="cuda").to(torch.bfloat16)
+    max_seq = max(lens) if max_seq is None else max_seq
+    ws = torch.empty(fk.flowkv_decode_attention_workspace(n, q_heads, geom.head_dim, max_seq,
+                                                          split), dtype=torch.uint8, device="cuda")
+    out = torch.full((n, q_heads, geom.head_dim), float("nan"), dtype=torch.float32, device="cuda")
+    scale = 1.0 / np.sqrt(geom.head_dim)
+    fk.flowkv_decode_attention(pool, layer, q, torch.as_tensor(tab, device="cuda"),
+                               torch.as_tensor(np.asarray(lens, np.int32), device="cuda"),
+                               max_seq, scale, out, ws, split)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.float64)
+    if not check:
+        return got, None
+    # oracle on a compact host copy of exactly the blocks the requests use
+    used = np.concatenate(tables)
+    host = download_blocks(pool, used)
+    lut = {int(b): i for i, b in enumerate(used)}
+    ctabs = [[lut[int(b)] for b in t] for t in tables]
+    want = decode_attention(host, bf16_to_f64(q), ctabs, [min(T, max_seq) for T in lens], layer,
+                            geom.kv_heads, geom.head_dim, scale)
+    vmax = max(float(t.abs().max()) for t in pool.tensors)
+    err = np.abs(got - want).max()
+    tol = 2e-4 * vmax + 1e-6
+    assert np.all(np.isfinite(got)), "non-finite output"
+    assert err <= tol, f"max error {err:.3e} > {tol:.3e}"
+    return got, err
+
+
+SHAPES = [  # (layers, kv heads, head dim, block size, q heads)
+    (2, 2, 64, 16, 4), (3, 1, 128, 16, 8), (2, 8, 128, 16, 32), (1, 4, 64, 5, 4),
+    (2, 2, 128, 1, 16), (4, 1, 64, 7, 1),
+]
+
+
+@pytest.mark.parametrize("seed", range(18))
+def test_random_cases_against_oracle(seed):
+    L, hkv, dh, bs, hq = SHAPES[seed % len(SHAPES)]
+    layout = (LM, BM)[seed % 2]
+    geom = Geometry(f"attn{seed}", L, hkv, dh, bs, "bfloat16")
+    g = np.random.default_rng(100 + seed)
+    n = int(g.integers(1, 5))
+    lens = [int(x) for x in g.integers(1, 700, size=n)]
+    if seed % 3 == 0:
+        lens[0] = 1
+    split = [0, 16, 64, 1, 300, 1024][seed % 6]
+    blocks = sum(max(1, -(-T // bs)) for T in lens) + int(g.integers(0, 20))
+    say(f"attn seed={seed} L={L} Hkv={hkv} Hq={hq} Dh={dh} bs={bs} {NAMES[layout]} "
+        f"lens={lens} split={split}")
+    _, err = run_case(geom, layout, blocks, lens, hq, seed, split)
+    say(f"  max error {err:.2e}")
+
+
+@pytest.mark.parametrize("layout", [BM, LM], ids=lambda x: NAMES[x])
+def test_llama8b_geometry_long_requests(layout):
+    """Llama-3-8B geometry (32 query heads on 8 KV heads, head_dim 128, block
+    16): requests of 1 to 20,000 tokens, ragged last blocks."""
+    geom = Geometry("llama8b", 32, 8, 128, 16, "bfloat16")
+    lens = [20000, 1, 13000, 4097, 16]
+    blocks = sum(-(-T // 16) for T in lens) + 64
+    say(f"8b attention {NAMES[layout]} lens={lens}")
+    _, err = run_case(geom, layout, blocks, lens, 32, 11, layer=17)
+    say(f"  max error {err:.2e}")
+
+
+def test_llama70b_share_geometry():
+    """One GPU's share of Llama-3-70B at TP=8: 1 KV head, 8 query heads."""
+    geom = Geometry("llama70b-tp8", 80, 1, 128, 16, "bfloat16")
+    lens = [32000, 777]
+    blocks = sum(-(-T // 16) for T in lens) + 16
+    _, err = run_case(geom, BM, blocks, lens, 8, 12, layer=79)
+    say(f"  max error {err:.2e}")
+
+
+def test_both_layouts_give_identical_outputs():
+    """The same K/V stored in the two Eq. 5 layouts gives bit-identical
+    outputs: the kernel's arithmetic does not depend on the layout."""
+    geom = Geometry("same", 4, 2, 128, 16, "bfloat16")
+    B, layer, hq = 60, 2, 8
+    bm = make_device_pool(geom, BM, B, "cuda", 9)[0]            # (B, L, 2, bs, Hkv, Dh)
+    lm = [bm[:, l].transpose(0, 1).contiguous() for l in range(geom.num_layers)]  # (2, B, ...)
+    pools = [fk.KVPool(BM, [bm]), fk.KVPool(LM, lm)]
+    lens = [333, 700]
+    tab = torch.as_tensor(np.array([np.arange(0, 44), np.arange(16, 60)], np.int32), device="cuda")
+    sl = torch.as_tensor(np.asarray(lens, np.int32), device="cuda")
+    q = torch.randn((2, hq, 128), device="cuda").to(torch.bfloat16)
+    outs = []
+    for pool in pools:
+        ws = torch.empty(fk.flowkv_decode_attention_workspace(2, hq, 128, 700), dtype=torch.uint8,
+                         device="cuda")
+        out = torch.empty((2, hq, 128), dtype=torch.float32, device="cuda")
+        fk.flowkv_decode_attention(pool, layer, q, tab, sl, 700, 0.088, out, ws)
+        torch.cuda.synchronize()
+        outs.append(out.cpu())
+    assert torch.equal(outs[0], outs[1])
+
+
+def test_length_caps_and_empty_request():
+    """Tokens past max_seq_len are not read; a zero-length request gives zeros."""
+    geom = Geometry("caps", 2, 2, 64, 16, "bfloat16")
+    got, err = run_case(geom, BM, 40, [300, 120], 4, 3, max_seq=200)
+    assert err is not None
+    z, _ = run_case(geom, LM, 40, [0, 50], 4, 4, check=False)
+    assert np.all(z[0] == 0)
