@@ -90,6 +90,8 @@ def parse():
     ap.add_argument("--unroll", type=int, default=0)
     ap.add_argument("--grid", type=int, default=0)
     ap.add_argument("--cache", type=int, default=0)
+    ap.add_argument("--split", type=int, default=0,
+                    help="attention: tokens per pass-1 workgroup (0 = library default)")
     ap.add_argument("--calibrate-copy-gib", type=float, default=1.0,
                     help="size of the plain copy run beside the kernel (HBM counter scale)")
     ap.add_argument("--calibration-only", action="store_true",
@@ -143,12 +145,14 @@ def bench_attention(args):
     out = torch.empty((len(lens), q_heads, geom.head_dim), dtype=torch.float32, device=dev)
     max_seq = int(lens.max())
     ws = torch.empty(fk.flowkv_decode_attention_workspace(len(lens), q_heads, geom.head_dim,
-                                                          max_seq), dtype=torch.uint8, device=dev)
+                                                          max_seq, args.split),
+                     dtype=torch.uint8, device=dev)
     scale = 1.0 / geom.head_dim ** 0.5
     layer = geom.num_layers // 2
 
     def step():
-        fk.flowkv_decode_attention(pool, layer, q, tab_d, lens_d, max_seq, scale, out, ws)
+        fk.flowkv_decode_attention(pool, layer, q, tab_d, lens_d, max_seq, scale, out, ws,
+                                   args.split)
 
     for _ in range(args.warmup):
         step()
@@ -167,8 +171,10 @@ def bench_attention(args):
     gc.enable()
     ms = statistics.fmean(a.elapsed_time(b) for a, b in evs)
     kv_bytes = int(lens.sum()) * 2 * geom.kv_heads * geom.head_dim * 2
-    splits = -(-max_seq // 256)
-    ws_bytes = 2 * len(lens) * q_heads * splits * (geom.head_dim + 2) * 4
+    split = args.split or fk.flowkv_decode_attention_split(len(lens), max_seq)
+    # workspace: written by pass 1 and read by pass 2, for the splits that exist
+    used_splits = int(sum(-(-int(T) // split) for T in lens))
+    ws_bytes = 2 * used_splits * q_heads * (geom.head_dim + 2) * 4
     algo = kv_bytes + q.numel() * 2 + out.numel() * 4 + ws_bytes + tab.nbytes
     achieved = algo / (ms * 1e-3) / 1e9
     line = {
@@ -181,7 +187,7 @@ def bench_attention(args):
                    "requests": len(lens), "tokens": int(lens.sum()), "q_heads": q_heads,
                    "kv_heads": geom.kv_heads, "head_dim": geom.head_dim,
                    "block_size": geom.block_size, "kv_dtype": "bf16",
-                   "layout": f"{args.layout}-major", "layer": layer},
+                   "layout": f"{args.layout}-major", "layer": layer, "split_tokens": split},
         "kernel_ms_avg": round(ms, 4),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None},

@@ -247,12 +247,21 @@ int flowkv_transfer_layers(const flowkv_pool* src, const flowkv_pool* dst,
 /* ---- decode attention over a pool (section 3.3: the PagedAttention kernel
         adapted to the restructured layout; the decode step of Eq. 2) -------- */
 
-#define FLOWKV_ATTN_DEFAULT_SPLIT 256 /* tokens per pass-1 workgroup */
-#define FLOWKV_ATTN_MAX_SPLIT 1024
+#define FLOWKV_ATTN_MAX_SPLIT 1024     /* most tokens per pass-1 workgroup    */
+#define FLOWKV_ATTN_MIN_AUTO_SPLIT 64  /* least tokens the default rule picks */
+#define FLOWKV_ATTN_AUTO_PAIRS 1024    /* (request, split) pairs it aims at   */
+
+/* The split length used when split_tokens is 0: the smallest power of two s
+   from FLOWKV_ATTN_MIN_AUTO_SPLIT to FLOWKV_ATTN_MAX_SPLIT with
+   n_req x ceil(max_seq_len / s) <= FLOWKV_ATTN_AUTO_PAIRS, else
+   FLOWKV_ATTN_MAX_SPLIT.  (Enough workgroups to fill the chip for one long
+   request; few enough splits that a large batch's merge stays small.)
+   Writes it to *split_tokens.  EINVAL for a NULL output or negative sizes. */
+int flowkv_decode_attention_split(int32_t n_req, int32_t max_seq_len, int32_t* split_tokens);
 
 /* Workspace bytes flowkv_decode_attention needs for n_req requests of at most
    max_seq_len tokens: n_req x q_heads x ceil(max_seq_len / split_tokens) x
-   (head_dim + 2) floats.  split_tokens 0 = FLOWKV_ATTN_DEFAULT_SPLIT. */
+   (head_dim + 2) floats, split_tokens 0 meaning the default rule above. */
 int flowkv_decode_attention_workspace(int32_t n_req, int32_t q_heads, int32_t head_dim,
                                       int32_t max_seq_len, int32_t split_tokens,
                                       int64_t* bytes);
@@ -271,7 +280,8 @@ int flowkv_decode_attention_workspace(int32_t n_req, int32_t q_heads, int32_t he
    max_blocks x block_size or beyond max_seq_len are not read; a block ID
    outside the pool contributes nothing; a request with no tokens gets zeros.
    head_dim 64 or 128; q_heads / kv_heads in {1, 2, 4, 8}; split_tokens 0 =
-   default, else 1..FLOWKV_ATTN_MAX_SPLIT.  Two launches on hip_stream.
+   the default rule (flowkv_decode_attention_split), else
+   1..FLOWKV_ATTN_MAX_SPLIT.  Two launches on hip_stream.
    EINVAL for bad shapes or pointers, ECAP for a short workspace. */
 int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer, const void* q_dev,
                             int32_t n_req, int32_t q_heads, int32_t kv_heads,

@@ -9,17 +9,30 @@
 // share Hkv KV heads, query head h reading KV head h / (Hq / Hkv).
 //
 // Decode attention reads every cached K and V element once and does ~2
-// flops per byte: it is HBM-bound, so it runs on the vector units (no MFMA).
+// flops per byte: it is HBM-bound, so it runs on the vector units (no MFMA),
+// and the work per token is kept small enough that the loads stay the limit.
 // Work split (flash-decoding style):
 //   pass 1: one workgroup per (KV head, token split, request).  A token's
-//           head vector (Dh bf16 = 256 B at Dh 128) is read by a group of
-//           Dh/8 lanes, 16 B each; the workgroup's groups take the split's
-//           tokens round-robin, `kTok` tokens in flight per group, and keep
-//           an online softmax (running max, sum, weighted V) per query head
-//           of the KV group in registers.  Groups merge through LDS and the
-//           workgroup writes its partial (max, sum, weighted V) per head.
-//   pass 2: one workgroup per (query head, request) merges the splits.
-// All arithmetic is float32; exponentials are exp2 of scores pre-scaled by
+//           head vector (Dh bf16) is read by one 16-lane DPP row, Dh/16
+//           values per lane; the workgroup's 16 rows take the split's tokens
+//           round-robin, kTok tokens per row per step.
+//           - q.k: bf16 pair dot products (v_dot2) on the raw bf16 values.
+//           - The kTok x G partial scores of a row are summed over its 16
+//             lanes by a transposed butterfly (row mirror, half mirror, two
+//             quad swaps): each step halves the values a lane holds, so the
+//             row ends with every (token, head) score owned by one lane
+//             (or replicated when there are fewer than 16).
+//           - The owner lane runs the online softmax for its score: a
+//             running reference max per head, moved only when a score
+//             exceeds it by more than 2^kLazy (so weights stay <= 2^kLazy and
+//             the weighted sums are rarely rescaled).
+//           - The weights and rescale factors go through a small LDS row
+//             buffer to all 16 lanes, which accumulate weight x V in float32.
+//           Rows merge through LDS and the workgroup writes its partial
+//           (reference max, sum, weighted V) per query head.
+//   pass 2: one workgroup per (query head, request) merges the splits,
+//           several splits per thread in flight.
+// All arithmetic is float32; exponentials are exp2 of scores scaled by
 // log2(e).  K and V are bfloat16; the output is float32.
 #include <hip/hip_runtime.h>
 
@@ -36,11 +49,24 @@ using flowkv::ok;
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(1))) u32x4 gvec;
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(1))) u32x4 gvec4;
+typedef __attribute__((address_space(1))) u32x2 gvec2;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kThreads = 256;       // pass-1 workgroup
-constexpr int kTok = 4;             // tokens in flight per lane group
+constexpr int kThreads = 256;              // pass-1 workgroup: 4 waves
+constexpr int kRowLanes = 16;              // lanes per token: one DPP row
+constexpr int kRows = kThreads / kRowLanes;
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLazy = 8.f;               // log2 of the largest unnormalised weight
+
+// DPP lane patterns inside a 16-lane row
+constexpr int kMirror = 0x140;             // lane i <- 15 - i
+constexpr int kHalfMirror = 0x141;         // lane i <- 7 - i within each half
+constexpr int kSwap1 = 0xB1;               // quad_perm [1,0,3,2]: i <- i ^ 1
+constexpr int kSwap2 = 0x4E;               // quad_perm [2,3,0,1]: i <- i ^ 2
+constexpr int kRor4 = 0x124;               // rotate the row by 4 lanes
+constexpr int kRor8 = 0x128;               // rotate the row by 8 lanes
 
 struct AttnArgs {
   const char* base[FLOWKV_MAX_LAYERS];  // pool tensors (layer-major) or base[0]
@@ -68,177 +94,361 @@ __device__ __forceinline__ int clamp_len(const AttnArgs& a, int T) {
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// Byte address of token slot `slot` of block b, K (kv 0) or V (kv 1), KV head
-// g, in the pool's layout (Eq. 5): the slot holds Hkv x Dh values, head-major.
-template <bool kLM, int kDh>
-__device__ __forceinline__ const char* kv_addr(const AttnArgs& a, int64_t b, int kv, int slot,
-                                               int g) {
-  const int64_t in_chunk = (int64_t(slot) * a.kv_heads + g) * kDh * 2;
-  if constexpr (kLM)
-    return a.base[a.layer] + (int64_t(kv) * a.pool_blocks + b) * a.chunk_bytes + in_chunk;
-  else
-    return a.base[0] + b * a.block_bytes + (int64_t(a.layer) * 2 + kv) * a.chunk_bytes +
-           in_chunk;
+// by value: a bit cast of a vector-element lvalue would read element 0
+__device__ __forceinline__ bf16x2 as_bf16x2(uint32_t w) { return __builtin_bit_cast(bf16x2, w); }
+
+template <int kCtrl>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), kCtrl, 0xF, 0xF, false));
 }
+
+// One butterfly step over partner pattern kCtrl.  With kN > 1 values the lane
+// keeps half of them (the upper half when `upper`), adding the partner's
+// copy of that half; the partner keeps the other half.  With one value it is
+// a plain pairwise sum.
+template <int kN, int kCtrl, int kP>
+__device__ __forceinline__ void fold(float (&v)[kP], bool upper) {
+  if constexpr (kN > 1) {
+#pragma unroll
+    for (int j = 0; j < kN / 2; ++j) {
+      const float lo = v[j], hi = v[j + kN / 2];
+      v[j] = (upper ? hi : lo) + dpp<kCtrl>(upper ? lo : hi);
+    }
+  } else {
+    v[0] += dpp<kCtrl>(v[0]);
+  }
+}
+
+template <int kW> struct Words;
+template <> struct Words<4> {
+  typedef u32x4 T;
+  static __device__ __forceinline__ T load_nt(const char* p) {
+    return __builtin_nontemporal_load((const gvec4*)p);
+  }
+};
+template <> struct Words<2> {
+  typedef u32x2 T;
+  static __device__ __forceinline__ T load_nt(const char* p) {
+    return __builtin_nontemporal_load((const gvec2*)p);
+  }
+};
 
 template <int kDh, int kG, bool kLM>
 __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) {
-  constexpr int kLPT = kDh / 8;                 // lanes per token (8 values each)
-  constexpr int kGroups = kThreads / kLPT;      // token groups per workgroup
+  constexpr int kW = kDh / 32;                  // bf16 pairs per lane (4 or 2)
+  constexpr int kV = 2 * kW;                    // K/V values per lane
+  constexpr int kTok = kG == 8 ? 2 : 4;         // tokens per row per step
+  constexpr int kLogTok = kTok == 4 ? 2 : 1;
+  constexpr int kP = kTok * kG;                 // partial scores per lane per step
+  constexpr int kR = kP > kRowLanes ? kP / kRowLanes : 1;  // scores a lane owns
+  constexpr int kCS = (kG + 3) / 4 * 4;         // rescale slots, padded to 16 B
+  constexpr int kXS = kP + kCS;                 // LDS row buffer: weights, rescales
+  constexpr int kStep = kRows * kTok;           // tokens per workgroup step
+  using VT = typename Words<kW>::T;
+
   const int g = blockIdx.x;                     // KV head
   const int split = blockIdx.y;
   const int r = blockIdx.z;
   const int tid = threadIdx.x;
-  const int grp = tid / kLPT;
-  const int lane = tid % kLPT;                  // which 8 values of the head vector
+  const int row = tid / kRowLanes;
+  const int lane = tid % kRowLanes;             // which kV values of the head vector
 
-  const int T = clamp_len(a, a.seq_lens[r]);
   const int t0 = split * a.split_tokens;
+  const int bs = a.block_size;
+  // the block IDs the split can touch, staged once in LDS: fetched without
+  // waiting for the request's length (a split of at most
+  // FLOWKV_ATTN_MAX_SPLIT tokens touches at most that many blocks plus one)
+  __shared__ int32_t s_blk[FLOWKV_ATTN_MAX_SPLIT + 1];
+  const int b0 = t0 / bs;
+  {
+    const int span = (t0 + a.split_tokens - 1) / bs - b0 + 1;
+    const int nb = span < a.max_blocks - b0 ? span : a.max_blocks - b0;
+    for (int i = tid; i < nb; i += kThreads)
+      s_blk[i] = a.tables[int64_t(r) * a.max_blocks + b0 + i];
+  }
+  const int T = clamp_len(a, a.seq_lens[r]);
   if (t0 >= T) return;  // uniform: this split is past the request's end
   const int t1 = t0 + a.split_tokens < T ? t0 + a.split_tokens : T;
 
-  // the split's block IDs, staged once in LDS (a split of at most
-  // FLOWKV_ATTN_MAX_SPLIT tokens touches at most that many blocks plus one)
-  __shared__ int32_t s_blk[FLOWKV_ATTN_MAX_SPLIT + 1];
-  const int b0 = t0 / a.block_size;
-  const int nb = (t1 - 1) / a.block_size - b0 + 1;
-  for (int i = tid; i < nb; i += kThreads) s_blk[i] = a.tables[int64_t(r) * a.max_blocks + b0 + i];
-
-  // this lane's 8 query values for each head of the KV group, pre-scaled
-  float q[kG][8];
+  // this lane's query pairs for each head of the KV group (raw bf16)
+  uint32_t q[kG][kW];
 #pragma unroll
   for (int h = 0; h < kG; ++h) {
-    const int qh = g * kG + h;
-    const u32x4 w = *reinterpret_cast<const u32x4*>(a.q + (int64_t(r) * a.q_heads + qh) * kDh +
-                                                    lane * 8);
+    const uint32_t* qp = reinterpret_cast<const uint32_t*>(
+        a.q + (int64_t(r) * a.q_heads + g * kG + h) * kDh + lane * kV);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      q[h][2 * j] = bf16_lo(w[j]) * a.scale_log2;
-      q[h][2 * j + 1] = bf16_hi(w[j]) * a.scale_log2;
-    }
+    for (int w = 0; w < kW; ++w) q[h][w] = qp[w];
+  }
+
+  // which partial score this lane owns after the butterfly: indices
+  // own .. own + kR - 1 of the (token u, head h) list, index u * kG + h
+  int own = 0;
+  {
+    int n = kP;
+    const int bits[4] = {8, 4, 1, 2};
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      if (n > 1) {
+        if (lane & bits[s]) own += n / 2;
+        n /= 2;
+      }
+  }
+  const int u_own = lane >> (4 - kLogTok);      // the owned scores' token
+
+  // pool addressing: K of (block b, slot) at kbase + b * bstride + slot *
+  // sstride + this lane's offset; V sits voff further
+  const char* kbase;
+  uint32_t bstride;
+  int64_t voff;
+  if constexpr (kLM) {
+    kbase = a.base[a.layer];
+    bstride = uint32_t(a.chunk_bytes);
+    voff = a.pool_blocks * a.chunk_bytes;
+  } else {
+    kbase = a.base[0] + int64_t(a.layer) * 2 * a.chunk_bytes;
+    bstride = uint32_t(a.block_bytes);
+    voff = a.chunk_bytes;
+  }
+  const uint32_t sstride = uint32_t(a.kv_heads) * kDh * 2;
+  kbase += g * kDh * 2 + lane * kV * 2;
+
+  // token bookkeeping per step slot u: token index, its block (relative to
+  // b0) and slot, advanced by kStep tokens per step without dividing
+  int tok[kTok], bi[kTok], sl[kTok];
+#pragma unroll
+  for (int u = 0; u < kTok; ++u) {
+    tok[u] = t0 + row + u * kRows;
+    bi[u] = tok[u] / bs - b0;
+    sl[u] = tok[u] % bs;
+  }
+  const int step_q = kStep / bs, step_r = kStep % bs;
+
+  __shared__ __attribute__((aligned(16))) float s_x[kRows][kXS];
+  float acc[kG][kV];
+#pragma unroll
+  for (int h = 0; h < kG; ++h)
+#pragma unroll
+    for (int v = 0; v < kV; ++v) acc[h][v] = 0.f;
+  float mref[kR], lsum[kR];
+#pragma unroll
+  for (int j = 0; j < kR; ++j) {
+    mref[j] = -INFINITY;
+    lsum[j] = 0.f;
   }
   __syncthreads();
 
-  float m[kG], l[kG], acc[kG][8];
-#pragma unroll
-  for (int h = 0; h < kG; ++h) {
-    m[h] = -INFINITY;
-    l[h] = 0.f;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[h][j] = 0.f;
-  }
-
-  for (int tb = t0 + grp; tb < t1; tb += kGroups * kTok) {
-    u32x4 kw[kTok], vw[kTok];
-    bool live[kTok];
+  for (int base = t0; base < t1; base += kStep) {
+    // K and V of each of the row's tokens that is in range and in the pool
+    // (others stay zero, with their live bit clear); then the bookkeeping
+    // advances one step.  (Issuing the next step's loads a step early
+    // measured no faster: the extra registers cost a wave per SIMD.)
+    VT kw[kTok], vw[kTok];
+    uint32_t live = 0;
 #pragma unroll
     for (int u = 0; u < kTok; ++u) {
-      const int t = tb + u * kGroups;
-      kw[u] = u32x4{0, 0, 0, 0};
-      vw[u] = u32x4{0, 0, 0, 0};
-      live[u] = t < t1;
-      if (live[u]) {
-        const int64_t b = s_blk[t / a.block_size - b0];
-        const bool in_pool = b >= 0 && b < a.pool_blocks;
-        live[u] = in_pool;
-        if (in_pool) {
-          const int slot = t % a.block_size;
-          kw[u] = __builtin_nontemporal_load((const gvec*)(kv_addr<kLM, kDh>(a, b, 0, slot, g)) +
-                                             lane);
-          vw[u] = __builtin_nontemporal_load((const gvec*)(kv_addr<kLM, kDh>(a, b, 1, slot, g)) +
-                                             lane);
+      kw[u] = VT{};
+      vw[u] = VT{};
+      if (tok[u] < t1) {
+        const int b = s_blk[bi[u]];
+        if (b >= 0 && b < a.pool_blocks) {
+          const char* kp = kbase + uint64_t(uint32_t(b)) * bstride + uint32_t(sl[u]) * sstride;
+          kw[u] = Words<kW>::load_nt(kp);
+          vw[u] = Words<kW>::load_nt(kp + voff);
+          live |= 1u << u;
         }
       }
-    }
-#pragma unroll
-    for (int u = 0; u < kTok; ++u) {
-      // the group's lanes all see the same `live`: t and b are per group
-      float k[8], v[8];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        k[2 * j] = bf16_lo(kw[u][j]);
-        k[2 * j + 1] = bf16_hi(kw[u][j]);
-        v[2 * j] = bf16_lo(vw[u][j]);
-        v[2 * j + 1] = bf16_hi(vw[u][j]);
+      tok[u] += kStep;
+      bi[u] += step_q;
+      sl[u] += step_r;
+      if (sl[u] >= bs) {
+        sl[u] -= bs;
+        bi[u] += 1;
       }
+    }
+
+    // partial q.k over this lane's values, index u * kG + h
+    float part[kP];
+#pragma unroll
+    for (int u = 0; u < kTok; ++u)
 #pragma unroll
       for (int h = 0; h < kG; ++h) {
         float s = 0.f;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) s = fmaf(q[h][j], k[j], s);
-        // sum over the group's lanes (they are consecutive, kLPT a power of 2)
-#pragma unroll
-        for (int off = kLPT / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, kLPT);
-        if (live[u]) {
-          const float m_new = fmaxf(m[h], s);
-          const float c = exp2f(m[h] - m_new);
-          const float p = exp2f(s - m_new);
-          l[h] = l[h] * c + p;
-#pragma unroll
-          for (int j = 0; j < 8; ++j) acc[h][j] = fmaf(acc[h][j], c, p * v[j]);
-          m[h] = m_new;
-        }
+        for (int w = 0; w < kW; ++w)
+          s = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(kw[u][w]), as_bf16x2(q[h][w]), s, false);
+        part[u * kG + h] = s;
       }
+    fold<kP, kMirror>(part, lane & 8);
+    fold<(kP / 2 > 1 ? kP / 2 : 1), kHalfMirror>(part, lane & 4);
+    fold<(kP / 4 > 1 ? kP / 4 : 1), kSwap1>(part, lane & 1);
+    fold<(kP / 8 > 1 ? kP / 8 : 1), kSwap2>(part, lane & 2);
+
+    // owner lanes: online softmax per owned (token, head)
+    const bool live_own = (live >> u_own) & 1u;
+#pragma unroll
+    for (int j = 0; j < kR; ++j) {
+      const float sc = live_own ? part[j] * a.scale_log2 : -INFINITY;
+      // the step's max over the kTok tokens of this head (lanes that differ
+      // only in their token bits)
+      float cm = sc;
+      if constexpr (kTok >= 4) cm = fmaxf(cm, dpp<kRor4>(cm));
+      cm = fmaxf(cm, dpp<kRor8>(cm));
+      float c = 1.f;
+      if (cm > mref[j] + kLazy) {  // also taken at the first live token (mref = -inf)
+        c = __builtin_amdgcn_exp2f(mref[j] - cm);
+        mref[j] = cm;
+      }
+      const float mu = mref[j] == -INFINITY ? 0.f : mref[j];
+      const float p = __builtin_amdgcn_exp2f(sc - mu);
+      lsum[j] = fmaf(lsum[j], c, p);
+      s_x[row][own + j] = p;
+      if (u_own == 0) s_x[row][kP + (own + j) % kG] = c;
     }
+    __builtin_amdgcn_wave_barrier();
+
+    // every lane: rescale, then accumulate weight x V
+    float px[kXS];
+#pragma unroll
+    for (int i = 0; i < kXS; i += 4) {
+      const float4 x4 = *reinterpret_cast<const float4*>(&s_x[row][i]);
+      px[i] = x4.x;
+      px[i + 1] = x4.y;
+      px[i + 2] = x4.z;
+      px[i + 3] = x4.w;
+    }
+    bool rescale = false;
+#pragma unroll
+    for (int h = 0; h < kG; ++h) rescale |= px[kP + h] != 1.f;
+    if (rescale) {
+#pragma unroll
+      for (int h = 0; h < kG; ++h)
+#pragma unroll
+        for (int v = 0; v < kV; ++v) acc[h][v] *= px[kP + h];
+    }
+#pragma unroll
+    for (int u = 0; u < kTok; ++u) {
+      float vf[kV];
+#pragma unroll
+      for (int w = 0; w < kW; ++w) {
+        vf[2 * w] = bf16_lo(vw[u][w]);
+        vf[2 * w + 1] = bf16_hi(vw[u][w]);
+      }
+#pragma unroll
+      for (int h = 0; h < kG; ++h)
+#pragma unroll
+        for (int v = 0; v < kV; ++v) acc[h][v] = fmaf(px[u * kG + h], vf[v], acc[h][v]);
+    }
+    __builtin_amdgcn_wave_barrier();
   }
 
-  // merge the token groups through LDS, one query head at a time; a group
-  // that saw no token has m = -inf and weighs nothing
-  __shared__ float s_m[kGroups];
-  __shared__ float s_l[kGroups];
-  __shared__ float s_acc[kGroups][kDh];
-  const int ngrp_used = (t1 - t0) < kGroups ? (t1 - t0) : kGroups;
+  // merge the rows: per head, a weight exp2(m_row - M) for each row's
+  // reference max m_row against the largest M; a row that saw no token has
+  // m_row = -inf and weighs nothing
+  __shared__ float s_m[kRows][kG], s_l[kRows][kG], s_w[kRows][kG];
+  __shared__ __attribute__((aligned(16))) float s_acc[kThreads / 64][kG][kDh];
+#pragma unroll
+  for (int j = 0; j < kR; ++j) {
+    float l = lsum[j];
+    if constexpr (kTok >= 4) l += dpp<kRor4>(l);
+    l += dpp<kRor8>(l);
+    if (u_own == 0) {
+      s_m[row][(own + j) % kG] = mref[j];
+      s_l[row][(own + j) % kG] = l;
+    }
+  }
+  __syncthreads();
+  float* const dst0 = a.ws + ((int64_t(r) * a.q_heads + g * kG) * a.max_splits + split) * (kDh + 2);
+  const int64_t head_stride = int64_t(a.max_splits) * (kDh + 2);
+  if (tid < kG) {
+    float M = -INFINITY;
+    for (int x = 0; x < kRows; ++x) M = fmaxf(M, s_m[x][tid]);
+    float L = 0.f;
+    for (int x = 0; x < kRows; ++x) {
+      const float w = s_m[x][tid] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s_m[x][tid] - M);
+      s_w[x][tid] = w;
+      L = fmaf(s_l[x][tid], w, L);
+    }
+    dst0[tid * head_stride] = M;
+    dst0[tid * head_stride + 1] = L;
+  }
+  __syncthreads();
+  // weight each row's sums, add the 4 rows of a wave, then the 4 waves
+  const int wave = tid / 64, row_in_wave = row % 4;
 #pragma unroll
   for (int h = 0; h < kG; ++h) {
-    if (lane == 0) {
-      s_m[grp] = m[h];
-      s_l[grp] = l[h];
-    }
+    const float w = s_w[row][h];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) s_acc[grp][lane * 8 + j] = acc[h][j];
-    __syncthreads();
-    for (int d = tid; d < kDh; d += kThreads) {
-      float M = -INFINITY;
-      for (int x = 0; x < ngrp_used; ++x) M = fmaxf(M, s_m[x]);
-      float L = 0.f, A = 0.f;
-      for (int x = 0; x < ngrp_used; ++x) {
-        const float w = s_m[x] == -INFINITY ? 0.f : exp2f(s_m[x] - M);
-        L = fmaf(s_l[x], w, L);
-        A = fmaf(s_acc[x][d], w, A);
-      }
-      float* dst =
-          a.ws + ((int64_t(r) * a.q_heads + g * kG + h) * a.max_splits + split) * (kDh + 2);
-      if (d == 0) {
-        dst[0] = M;
-        dst[1] = L;
-      }
-      dst[2 + d] = A;
+    for (int v = 0; v < kV; ++v) {
+      float x = acc[h][v] * w;
+      x += __shfl_xor(x, 16);
+      x += __shfl_xor(x, 32);
+      if (row_in_wave == 0) s_acc[wave][h][lane * kV + v] = x;
     }
-    __syncthreads();
+  }
+  __syncthreads();
+  for (int i = tid; i < kG * kDh; i += kThreads) {
+    const int h = i / kDh, d = i % kDh;
+    float A = 0.f;
+#pragma unroll
+    for (int x = 0; x < kThreads / 64; ++x) A += s_acc[x][h][d];
+    dst0[h * head_stride + 2 + d] = A;
   }
 }
 
+// Pass 2: one workgroup per (query head, request).  The largest split
+// reference comes first (all threads over the splits, then across the
+// workgroup); then 256 / Dh thread sets each take every (256 / Dh)-th split,
+// eight splits' loads in flight per thread, and the sets' sums meet in LDS.
+constexpr int kMergeThreads = 256;
+
 template <int kDh>
-__global__ __launch_bounds__(kDh) void decode_attn_merge(const AttnArgs a) {
-  const int h = blockIdx.x, r = blockIdx.y, d = threadIdx.x;
+__global__ __launch_bounds__(kMergeThreads) void decode_attn_merge(const AttnArgs a) {
+  constexpr int kParts = kMergeThreads / kDh;
+  const int h = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
+  const int d = tid % kDh, part = tid / kDh;
   const int T = clamp_len(a, a.seq_lens[r]);
   float* o = a.out + (int64_t(r) * a.q_heads + h) * kDh;
   if (T <= 0) {
-    o[d] = 0.f;
+    if (part == 0) o[d] = 0.f;
     return;
   }
   const int ns = (T + a.split_tokens - 1) / a.split_tokens;
   const float* src = a.ws + (int64_t(r) * a.q_heads + h) * a.max_splits * (kDh + 2);
+
+  __shared__ float s_red[kMergeThreads / 64];
   float M = -INFINITY;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, src[s * (kDh + 2)]);
+  for (int x = tid; x < ns; x += kMergeThreads) M = fmaxf(M, src[int64_t(x) * (kDh + 2)]);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+  if (tid % 64 == 0) s_red[tid / 64] = M;
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < kMergeThreads / 64; ++w) M = fmaxf(M, s_red[w]);
+
   float L = 0.f, A = 0.f;
-  for (int s = 0; s < ns; ++s) {
-    const float ms = src[s * (kDh + 2)];
+#pragma unroll 8
+  for (int x = part; x < ns; x += kParts) {
+    const float* e = src + int64_t(x) * (kDh + 2);
+    const float ms = e[0];
     const float w = ms == -INFINITY ? 0.f : exp2f(ms - M);
-    L = fmaf(src[s * (kDh + 2) + 1], w, L);
-    A = fmaf(src[s * (kDh + 2) + 2 + d], w, A);
+    L = fmaf(e[1], w, L);
+    A = fmaf(e[2 + d], w, A);
   }
-  o[d] = L > 0.f ? A / L : 0.f;
+  __shared__ float s_a[kParts][kDh];
+  __shared__ float s_l[kParts];
+  s_a[part][d] = A;
+  if (d == 0) s_l[part] = L;
+  __syncthreads();
+  if (part == 0) {
+    float At = 0.f, Lt = 0.f;
+#pragma unroll
+    for (int p = 0; p < kParts; ++p) {
+      At += s_a[p][d];
+      Lt += s_l[p];
+    }
+    o[d] = Lt > 0.f ? At / Lt : 0.f;
+  }
 }
 
 using SplitFn = void (*)(AttnArgs);
@@ -258,6 +468,12 @@ SplitFn pick_split(int D, int G, bool lm) {
   return lm ? pick_group<128, true>(G) : pick_group<128, false>(G);
 }
 
+int32_t auto_split(int32_t n_req, int32_t max_seq_len) {
+  for (int32_t s = FLOWKV_ATTN_MIN_AUTO_SPLIT; s < FLOWKV_ATTN_MAX_SPLIT; s *= 2)
+    if (int64_t(n_req) * ((int64_t(max_seq_len) + s - 1) / s) <= FLOWKV_ATTN_AUTO_PAIRS) return s;
+  return FLOWKV_ATTN_MAX_SPLIT;
+}
+
 int64_t ws_bytes(int32_t n_req, int32_t q_heads, int32_t head_dim, int32_t max_seq_len,
                  int32_t split_tokens) {
   const int64_t splits = (int64_t(max_seq_len) + split_tokens - 1) / split_tokens;
@@ -266,13 +482,21 @@ int64_t ws_bytes(int32_t n_req, int32_t q_heads, int32_t head_dim, int32_t max_s
 
 }  // namespace
 
+extern "C" int flowkv_decode_attention_split(int32_t n_req, int32_t max_seq_len,
+                                             int32_t* split_tokens) {
+  if (!split_tokens) return fail(FLOWKV_EINVAL, "NULL output");
+  if (n_req < 0 || max_seq_len < 0) return fail(FLOWKV_EINVAL, "negative sizes");
+  *split_tokens = auto_split(n_req, max_seq_len);
+  return ok();
+}
+
 extern "C" int flowkv_decode_attention_workspace(int32_t n_req, int32_t q_heads,
                                                  int32_t head_dim, int32_t max_seq_len,
                                                  int32_t split_tokens, int64_t* bytes) {
   if (!bytes) return fail(FLOWKV_EINVAL, "NULL output");
   if (n_req < 0 || q_heads < 1 || head_dim < 1 || max_seq_len < 0)
     return fail(FLOWKV_EINVAL, "bad attention shape");
-  if (split_tokens == 0) split_tokens = FLOWKV_ATTN_DEFAULT_SPLIT;
+  if (split_tokens == 0) split_tokens = auto_split(n_req, max_seq_len);
   if (split_tokens < 1 || split_tokens > FLOWKV_ATTN_MAX_SPLIT)
     return fail(FLOWKV_EINVAL, "split_tokens %d: need 1..%d", split_tokens,
                 FLOWKV_ATTN_MAX_SPLIT);
@@ -308,9 +532,15 @@ extern "C" int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer,
     return fail(FLOWKV_EINVAL, "chunk_bytes %lld is not block_size x %d KV heads x %d bf16",
                 (long long)pool->chunk_bytes, kv_heads, head_dim);
   const int64_t bs = pool->chunk_bytes / per_token;
+  // the kernel forms block offsets in 32 bits: one block stride under 4 GiB
+  const int64_t stride = pool->layout == FLOWKV_LAYOUT_LAYER_MAJOR
+                             ? pool->chunk_bytes
+                             : 2 * int64_t(pool->num_layers) * pool->chunk_bytes;
+  if (stride >= (int64_t(1) << 32))
+    return fail(FLOWKV_EINVAL, "block stride of %lld bytes: need under 4 GiB", (long long)stride);
   if (n_req < 0 || max_blocks < 0 || max_seq_len < 0)
     return fail(FLOWKV_EINVAL, "negative sizes");
-  if (split_tokens == 0) split_tokens = FLOWKV_ATTN_DEFAULT_SPLIT;
+  if (split_tokens == 0) split_tokens = auto_split(n_req, max_seq_len);
   if (split_tokens < 1 || split_tokens > FLOWKV_ATTN_MAX_SPLIT)
     return fail(FLOWKV_EINVAL, "split_tokens %d: need 1..%d", split_tokens,
                 FLOWKV_ATTN_MAX_SPLIT);
@@ -362,7 +592,7 @@ extern "C" int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer,
   if (e == hipSuccess) {
     const void* merge = head_dim == 64 ? reinterpret_cast<const void*>(decode_attn_merge<64>)
                                        : reinterpret_cast<const void*>(decode_attn_merge<128>);
-    e = hipLaunchKernel(merge, dim3(unsigned(q_heads), unsigned(n_req)), dim3(unsigned(head_dim)),
+    e = hipLaunchKernel(merge, dim3(unsigned(q_heads), unsigned(n_req)), dim3(kMergeThreads),
                         args, 0, st);
   }
   if (e == hipSuccess) e = hipGetLastError();

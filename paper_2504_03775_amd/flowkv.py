@@ -88,6 +88,8 @@ SIGNATURES = {
                                               ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                               ctypes.POINTER(flowkv_launch_config),
                                               ctypes.c_void_p]),
+    "flowkv_decode_attention_split": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32,
+                                                     ctypes.POINTER(ctypes.c_int32)]),
     "flowkv_decode_attention_workspace": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32,
                                                          ctypes.c_int32, ctypes.c_int32,
                                                          ctypes.c_int32, _I64P]),
@@ -345,6 +347,14 @@ def flowkv_transfer_layers(src: KVPool, dst: KVPool, segs_dev, n_segs: int, tota
                                        n_segs, total_blocks, layer_begin, layer_count,
                                        ctypes.byref(cfg), ctypes.c_void_p(_stream_handle(stream))),
            "flowkv_transfer_layers")
+
+
+def flowkv_decode_attention_split(n_req: int, max_seq_len: int) -> int:
+    """The split length flowkv_decode_attention uses when split_tokens is 0."""
+    s = ctypes.c_int32()
+    _check(_lib.flowkv_decode_attention_split(n_req, max_seq_len, ctypes.byref(s)),
+           "flowkv_decode_attention_split")
+    return s.value
 
 
 def flowkv_decode_attention_workspace(n_req: int, q_heads: int, head_dim: int,

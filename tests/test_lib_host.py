@@ -37,6 +37,35 @@ def test_library_exports_every_declared_function():
     assert set(names) == set(fk.SIGNATURES)
 
 
+def test_binding_constants_match_the_header():
+    text = open(os.path.join(ROOT, "include", "flowkv.h")).read()
+    defines = dict(re.findall(r"#define\s+(FLOWKV_\w+)\s+(-?\d+)", text))
+    assert int(defines["FLOWKV_INLINE_RUNS"]) == fk.INLINE_RUNS
+    enums = dict(re.findall(r"\b(FLOWKV_E?\w+)\s*=\s*(-?\d+)", text))
+    for name in ("OK", "EINVAL", "ENOSPC", "ERANGE", "EDUP", "ECAP", "EHIP"):
+        assert int(enums["FLOWKV_" + name]) == getattr(fk, name), name
+
+
+def test_attention_split_rule_and_workspace():
+    """The default split: the smallest power of two from 64 to 1024 giving at
+    most 1024 (request, split) pairs; the workspace follows it."""
+    cases = {(1, 13000): 64, (1, 200000): 256, (32, 20000): 1024, (8, 8192): 64,
+             (9, 8192): 128, (0, 5): 64, (3, 0): 64, (2000, 100): 1024}
+    for (n, T), want in cases.items():
+        got = fk.flowkv_decode_attention_split(n, T)
+        assert got == want, (n, T, got)
+        brute = next((s for s in (64, 128, 256, 512) if n * -(-T // s) <= 1024), 1024)
+        assert got == brute
+        ws = fk.flowkv_decode_attention_workspace(n, 32, 128, T)
+        assert ws == n * 32 * -(-T // got) * 130 * 4
+    assert fk.flowkv_decode_attention_workspace(2, 8, 64, 1000, 100) == 2 * 8 * 10 * 66 * 4
+    for bad in ((-1, 5), (1, -5)):
+        with pytest.raises(fk.FlowKVError):
+            fk.flowkv_decode_attention_split(*bad)
+    with pytest.raises(fk.FlowKVError):
+        fk.flowkv_decode_attention_workspace(1, 8, 128, 100, 1025)
+
+
 def test_strerror_names_every_code():
     for c in (fk.OK, fk.EINVAL, fk.ENOSPC, fk.ERANGE, fk.EDUP, fk.ECAP, fk.EHIP):
         assert fk.strerror(c) and fk.strerror(c) != "unknown status code"
