@@ -90,6 +90,10 @@ def parse():
     ap.add_argument("--unroll", type=int, default=0)
     ap.add_argument("--grid", type=int, default=0)
     ap.add_argument("--cache", type=int, default=0)
+    ap.add_argument("--attn-workload", choices=["batch", "8b", "70b"], default="batch",
+                    help="attention: receiver pool and block lists of the batch (32 requests), "
+                         "8b (one 13,000-token request) or 70b (the TP=8 share, 16 x 32,000 "
+                         "tokens) workload")
     ap.add_argument("--split", type=int, default=0,
                     help="attention: tokens per pass-1 workgroup (0 = library default)")
     ap.add_argument("--calibrate-copy-gib", type=float, default=1.0,
@@ -117,10 +121,20 @@ def traffic_from_profile():
     return float(t.group(1)) if t else None
 
 
+ATTN_WORKLOADS = {
+    # name: (recipe, args, query heads, workload label)
+    "batch": ("batch32", ("segment",), 32, "llama3-8b-decode-attention-batch-32-requests-2k-20k"),
+    "8b": ("llama8b_13k", ("segment",), 32, "llama3-8b-decode-attention-one-13k-request"),
+    "70b": ("llama70b_tp8", ("segment",), 8, "llama3-70b-tp8-share-decode-attention-16x32k"),
+}
+
+
 def bench_attention(args):
     """Decode attention (one layer, one new token per request) over the
-    receiver pool of the 32-request batch workload: 32 query heads on 8 KV
-    heads, head_dim 128, block 16, 2,000-20,000 tokens per request."""
+    receiver pool and block lists of a transfer workload: by default the
+    32-request batch (32 query heads on 8 KV heads, head_dim 128, block 16,
+    2,000-20,000 tokens per request); also the 13,000-token request and one
+    GPU's share of Llama-3-70B at TP=8 (8 query heads on 1 KV head)."""
     import numpy as np
     import torch
 
@@ -130,9 +144,9 @@ def bench_attention(args):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     layout = fk.LAYOUT_BLOCK_MAJOR if args.layout == "block" else fk.LAYOUT_LAYER_MAJOR
-    wl = recipes.batch32(lambda P, pol, seed: fk.Allocator(P, pol, seed), "segment")
+    recipe, rargs, q_heads, label = ATTN_WORKLOADS[args.attn_workload]
+    wl = getattr(recipes, recipe)(lambda P, pol, seed: fk.Allocator(P, pol, seed), *rargs)
     geom = wl.geom
-    q_heads = 32
     pool = fk.KVPool(layout, make_device_pool(geom, layout, wl.dst_pool_blocks, dev, seed=1))
     lens = np.asarray(wl.tokens, dtype=np.int32)
     max_blocks = max(len(d) for _, d in wl.tables)
@@ -183,7 +197,7 @@ def bench_attention(args):
         "warmup": args.warmup, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "llama3-8b-decode-attention-batch-32-requests-2k-20k",
+        "config": {"workload": label,
                    "requests": len(lens), "tokens": int(lens.sum()), "q_heads": q_heads,
                    "kv_heads": geom.kv_heads, "head_dim": geom.head_dim,
                    "block_size": geom.block_size, "kv_dtype": "bf16",

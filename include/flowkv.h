@@ -248,14 +248,15 @@ int flowkv_transfer_layers(const flowkv_pool* src, const flowkv_pool* dst,
         adapted to the restructured layout; the decode step of Eq. 2) -------- */
 
 #define FLOWKV_ATTN_MAX_SPLIT 1024     /* most tokens per pass-1 workgroup    */
-#define FLOWKV_ATTN_MIN_AUTO_SPLIT 64  /* least tokens the default rule picks */
-#define FLOWKV_ATTN_AUTO_PAIRS 1024    /* (request, split) pairs it aims at   */
+#define FLOWKV_ATTN_MIN_AUTO_SPLIT 256 /* least tokens the default rule picks */
+#define FLOWKV_ATTN_AUTO_PAIRS 512     /* (request, split) pairs it aims at   */
 
 /* The split length used when split_tokens is 0: the smallest power of two s
    from FLOWKV_ATTN_MIN_AUTO_SPLIT to FLOWKV_ATTN_MAX_SPLIT with
    n_req x ceil(max_seq_len / s) <= FLOWKV_ATTN_AUTO_PAIRS, else
-   FLOWKV_ATTN_MAX_SPLIT.  (Enough workgroups to fill the chip for one long
-   request; few enough splits that a large batch's merge stays small.)
+   FLOWKV_ATTN_MAX_SPLIT.  (Long splits amortise each workgroup's start-up
+   and keep the merge small; a long request still gets tens of splits per
+   KV head.)
    Writes it to *split_tokens.  EINVAL for a NULL output or negative sizes. */
 int flowkv_decode_attention_split(int32_t n_req, int32_t max_seq_len, int32_t* split_tokens);
 

@@ -15,7 +15,7 @@
 //   pass 1: one workgroup per (KV head, token split, request).  A token's
 //           head vector (Dh bf16) is read by one 16-lane DPP row, Dh/16
 //           values per lane; the workgroup's 16 rows take the split's tokens
-//           round-robin, kTok tokens per row per step.
+//           round-robin, 4 tokens per row per step.
 //           - q.k: bf16 pair dot products (v_dot2) on the raw bf16 values.
 //           - The kTok x G partial scores of a row are summed over its 16
 //             lanes by a transposed butterfly (row mirror, half mirror, two
@@ -138,13 +138,19 @@ template <int kDh, int kG, bool kLM>
 __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) {
   constexpr int kW = kDh / 32;                  // bf16 pairs per lane (4 or 2)
   constexpr int kV = 2 * kW;                    // K/V values per lane
-  constexpr int kTok = kG == 8 ? 2 : 4;         // tokens per row per step
-  constexpr int kLogTok = kTok == 4 ? 2 : 1;
-  constexpr int kP = kTok * kG;                 // partial scores per lane per step
+  constexpr int kTok = 4;                       // tokens per row per step
+  // With 8 query heads per KV head, two rows share each token, 4 heads each:
+  // a lane then holds the state of 4 heads (the registers of 4 waves per
+  // SIMD instead of 2); the pair's loads of the same token fall in one wave
+  // instruction and cost no extra HBM traffic.
+  constexpr int kHS = kG == 8 ? 2 : 1;          // rows per token
+  constexpr int kGl = kG / kHS;                 // query heads per row
+  constexpr int kTG = kRows / kHS;              // token groups per workgroup
+  constexpr int kP = kTok * kGl;                // partial scores per lane per step
   constexpr int kR = kP > kRowLanes ? kP / kRowLanes : 1;  // scores a lane owns
-  constexpr int kCS = (kG + 3) / 4 * 4;         // rescale slots, padded to 16 B
+  constexpr int kCS = (kGl + 3) / 4 * 4;        // rescale slots, padded to 16 B
   constexpr int kXS = kP + kCS;                 // LDS row buffer: weights, rescales
-  constexpr int kStep = kRows * kTok;           // tokens per workgroup step
+  constexpr int kStep = kTG * kTok;             // tokens per workgroup step
   using VT = typename Words<kW>::T;
 
   const int g = blockIdx.x;                     // KV head
@@ -153,6 +159,8 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
   const int tid = threadIdx.x;
   const int row = tid / kRowLanes;
   const int lane = tid % kRowLanes;             // which kV values of the head vector
+  const int tg = row / kHS;                     // the row's token group
+  const int hh = row % kHS;                     // and its share of the heads
 
   const int t0 = split * a.split_tokens;
   const int bs = a.block_size;
@@ -171,18 +179,19 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
   if (t0 >= T) return;  // uniform: this split is past the request's end
   const int t1 = t0 + a.split_tokens < T ? t0 + a.split_tokens : T;
 
-  // this lane's query pairs for each head of the KV group (raw bf16)
-  uint32_t q[kG][kW];
+  // this lane's query pairs for each of the row's heads (raw bf16)
+  const int h0 = g * kG + hh * kGl;             // the row's first query head
+  uint32_t q[kGl][kW];
 #pragma unroll
-  for (int h = 0; h < kG; ++h) {
+  for (int h = 0; h < kGl; ++h) {
     const uint32_t* qp = reinterpret_cast<const uint32_t*>(
-        a.q + (int64_t(r) * a.q_heads + g * kG + h) * kDh + lane * kV);
+        a.q + (int64_t(r) * a.q_heads + h0 + h) * kDh + lane * kV);
 #pragma unroll
     for (int w = 0; w < kW; ++w) q[h][w] = qp[w];
   }
 
   // which partial score this lane owns after the butterfly: indices
-  // own .. own + kR - 1 of the (token u, head h) list, index u * kG + h
+  // own .. own + kR - 1 of the (token u, head h) list, index u * kGl + h
   int own = 0;
   {
     int n = kP;
@@ -194,7 +203,7 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
         n /= 2;
       }
   }
-  const int u_own = lane >> (4 - kLogTok);      // the owned scores' token
+  const int u_own = own / kGl;                  // the owned scores' token
 
   // pool addressing: K of (block b, slot) at kbase + b * bstride + slot *
   // sstride + this lane's offset; V sits voff further
@@ -218,16 +227,16 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
   int tok[kTok], bi[kTok], sl[kTok];
 #pragma unroll
   for (int u = 0; u < kTok; ++u) {
-    tok[u] = t0 + row + u * kRows;
+    tok[u] = t0 + tg + u * kTG;
     bi[u] = tok[u] / bs - b0;
     sl[u] = tok[u] % bs;
   }
   const int step_q = kStep / bs, step_r = kStep % bs;
 
   __shared__ __attribute__((aligned(16))) float s_x[kRows][kXS];
-  float acc[kG][kV];
+  float acc[kGl][kV];
 #pragma unroll
-  for (int h = 0; h < kG; ++h)
+  for (int h = 0; h < kGl; ++h)
 #pragma unroll
     for (int v = 0; v < kV; ++v) acc[h][v] = 0.f;
   float mref[kR], lsum[kR];
@@ -242,22 +251,23 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
     // K and V of each of the row's tokens that is in range and in the pool
     // (others stay zero, with their live bit clear); then the bookkeeping
     // advances one step.  (Issuing the next step's loads a step early
-    // measured no faster: the extra registers cost a wave per SIMD.)
+    // measured slower: its registers cost waves.)
     VT kw[kTok], vw[kTok];
     uint32_t live = 0;
 #pragma unroll
     for (int u = 0; u < kTok; ++u) {
-      kw[u] = VT{};
-      vw[u] = VT{};
-      if (tok[u] < t1) {
-        const int b = s_blk[bi[u]];
-        if (b >= 0 && b < a.pool_blocks) {
-          const char* kp = kbase + uint64_t(uint32_t(b)) * bstride + uint32_t(sl[u]) * sstride;
-          kw[u] = Words<kW>::load_nt(kp);
-          vw[u] = Words<kW>::load_nt(kp + voff);
-          live |= 1u << u;
-        }
-      }
+      // branch-free, so the loads' count is static: a token past the split's
+      // end or with a block outside the pool reads the pool's first slot
+      // instead, and its V is zeroed (its score is replaced by -inf below)
+      const bool in = tok[u] < t1;
+      const int b = s_blk[in ? bi[u] : 0];
+      const bool ok = in && b >= 0 && b < a.pool_blocks;
+      const char* kp =
+          kbase + (ok ? uint64_t(uint32_t(b)) * bstride + uint32_t(sl[u]) * sstride : uint64_t(0));
+      kw[u] = Words<kW>::load_nt(kp);
+      vw[u] = Words<kW>::load_nt(kp + voff);
+      if (!ok) vw[u] = VT{};
+      live |= uint32_t(ok) << u;
       tok[u] += kStep;
       bi[u] += step_q;
       sl[u] += step_r;
@@ -267,17 +277,17 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
       }
     }
 
-    // partial q.k over this lane's values, index u * kG + h
+    // partial q.k over this lane's values, index u * kGl + h
     float part[kP];
 #pragma unroll
     for (int u = 0; u < kTok; ++u)
 #pragma unroll
-      for (int h = 0; h < kG; ++h) {
+      for (int h = 0; h < kGl; ++h) {
         float s = 0.f;
 #pragma unroll
         for (int w = 0; w < kW; ++w)
           s = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(kw[u][w]), as_bf16x2(q[h][w]), s, false);
-        part[u * kG + h] = s;
+        part[u * kGl + h] = s;
       }
     fold<kP, kMirror>(part, lane & 8);
     fold<(kP / 2 > 1 ? kP / 2 : 1), kHalfMirror>(part, lane & 4);
@@ -289,10 +299,9 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
 #pragma unroll
     for (int j = 0; j < kR; ++j) {
       const float sc = live_own ? part[j] * a.scale_log2 : -INFINITY;
-      // the step's max over the kTok tokens of this head (lanes that differ
-      // only in their token bits)
-      float cm = sc;
-      if constexpr (kTok >= 4) cm = fmaxf(cm, dpp<kRor4>(cm));
+      // the step's max over the 4 tokens of this head: the lanes holding
+      // them differ only in lane bits 2 and 3
+      float cm = fmaxf(sc, dpp<kRor4>(sc));
       cm = fmaxf(cm, dpp<kRor8>(cm));
       float c = 1.f;
       if (cm > mref[j] + kLazy) {  // also taken at the first live token (mref = -inf)
@@ -303,7 +312,7 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
       const float p = __builtin_amdgcn_exp2f(sc - mu);
       lsum[j] = fmaf(lsum[j], c, p);
       s_x[row][own + j] = p;
-      if (u_own == 0) s_x[row][kP + (own + j) % kG] = c;
+      if (u_own == 0) s_x[row][kP + (own + j) % kGl] = c;
     }
     __builtin_amdgcn_wave_barrier();
 
@@ -319,10 +328,10 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
     }
     bool rescale = false;
 #pragma unroll
-    for (int h = 0; h < kG; ++h) rescale |= px[kP + h] != 1.f;
+    for (int h = 0; h < kGl; ++h) rescale |= px[kP + h] != 1.f;
     if (rescale) {
 #pragma unroll
-      for (int h = 0; h < kG; ++h)
+      for (int h = 0; h < kGl; ++h)
 #pragma unroll
         for (int v = 0; v < kV; ++v) acc[h][v] *= px[kP + h];
     }
@@ -335,55 +344,57 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
         vf[2 * w + 1] = bf16_hi(vw[u][w]);
       }
 #pragma unroll
-      for (int h = 0; h < kG; ++h)
+      for (int h = 0; h < kGl; ++h)
 #pragma unroll
-        for (int v = 0; v < kV; ++v) acc[h][v] = fmaf(px[u * kG + h], vf[v], acc[h][v]);
+        for (int v = 0; v < kV; ++v) acc[h][v] = fmaf(px[u * kGl + h], vf[v], acc[h][v]);
     }
     __builtin_amdgcn_wave_barrier();
   }
 
-  // merge the rows: per head, a weight exp2(m_row - M) for each row's
-  // reference max m_row against the largest M; a row that saw no token has
-  // m_row = -inf and weighs nothing
-  __shared__ float s_m[kRows][kG], s_l[kRows][kG], s_w[kRows][kG];
+  // merge the rows that share heads: per head, a weight exp2(m_row - M) for
+  // each row's reference max m_row against the largest M; a row that saw no
+  // token has m_row = -inf and weighs nothing
+  __shared__ float s_m[kRows][kGl], s_l[kRows][kGl], s_w[kRows][kGl];
   __shared__ __attribute__((aligned(16))) float s_acc[kThreads / 64][kG][kDh];
 #pragma unroll
   for (int j = 0; j < kR; ++j) {
     float l = lsum[j];
-    if constexpr (kTok >= 4) l += dpp<kRor4>(l);
+    l += dpp<kRor4>(l);
     l += dpp<kRor8>(l);
     if (u_own == 0) {
-      s_m[row][(own + j) % kG] = mref[j];
-      s_l[row][(own + j) % kG] = l;
+      s_m[row][(own + j) % kGl] = mref[j];
+      s_l[row][(own + j) % kGl] = l;
     }
   }
   __syncthreads();
   float* const dst0 = a.ws + ((int64_t(r) * a.q_heads + g * kG) * a.max_splits + split) * (kDh + 2);
   const int64_t head_stride = int64_t(a.max_splits) * (kDh + 2);
-  if (tid < kG) {
+  if (tid < kG) {  // thread = query head of the group: rows x with x % kHS == its share
+    const int sh = tid / kGl, h = tid % kGl;
     float M = -INFINITY;
-    for (int x = 0; x < kRows; ++x) M = fmaxf(M, s_m[x][tid]);
+    for (int x = sh; x < kRows; x += kHS) M = fmaxf(M, s_m[x][h]);
     float L = 0.f;
-    for (int x = 0; x < kRows; ++x) {
-      const float w = s_m[x][tid] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s_m[x][tid] - M);
-      s_w[x][tid] = w;
-      L = fmaf(s_l[x][tid], w, L);
+    for (int x = sh; x < kRows; x += kHS) {
+      const float w = s_m[x][h] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s_m[x][h] - M);
+      s_w[x][h] = w;
+      L = fmaf(s_l[x][h], w, L);
     }
     dst0[tid * head_stride] = M;
     dst0[tid * head_stride + 1] = L;
   }
   __syncthreads();
-  // weight each row's sums, add the 4 rows of a wave, then the 4 waves
+  // weight each row's sums, add the rows of a wave that share heads (lane
+  // distance 16 x kHS), then the 4 waves
   const int wave = tid / 64, row_in_wave = row % 4;
 #pragma unroll
-  for (int h = 0; h < kG; ++h) {
+  for (int h = 0; h < kGl; ++h) {
     const float w = s_w[row][h];
 #pragma unroll
     for (int v = 0; v < kV; ++v) {
       float x = acc[h][v] * w;
-      x += __shfl_xor(x, 16);
+      if constexpr (kHS == 1) x += __shfl_xor(x, 16);
       x += __shfl_xor(x, 32);
-      if (row_in_wave == 0) s_acc[wave][h][lane * kV + v] = x;
+      if (row_in_wave < kHS) s_acc[wave][hh * kGl + h][lane * kV + v] = x;
     }
   }
   __syncthreads();

@@ -156,3 +156,50 @@ def test_length_caps_and_empty_request():
     assert err is not None
     z, _ = run_case(geom, LM, 40, [0, 50], 4, 4, check=False)
     assert np.all(z[0] == 0)
+
+
+@pytest.mark.parametrize("layout", [BM, LM], ids=lambda x: NAMES[x])
+def test_blocks_outside_the_pool_contribute_nothing(layout):
+    """A block ID outside the pool (negative or >= the pool's size) inside a
+    request's length is skipped: the output equals attention over the tokens
+    of the valid blocks alone (attention does not depend on token order)."""
+    geom = Geometry("holes", 3, 2, 128, 16, "bfloat16")
+    B, layer, hq, bs = 50, 1, 8, 16
+    pool = fk.KVPool(layout, make_device_pool(geom, layout, B, "cuda", 21))
+    g = np.random.default_rng(21)
+    perm = g.permutation(B).astype(np.int32)
+    full = [perm[0:10], perm[10:30]]           # 10 and 20 blocks
+    lens = [10 * bs - 5, 20 * bs - 9]          # ragged last blocks
+    holes = [[3], [0, 7, 8, 15]]               # positions replaced, never the last block
+    bad = [-1, B, B + 1000, -7]
+    tab = np.full((2, 20), -1, dtype=np.int32)
+    valid_tables, valid_lens = [], []
+    for r in range(2):
+        t = full[r].copy()
+        for i, pos in enumerate(holes[r]):
+            t[pos] = bad[i % len(bad)]
+        tab[r, :len(t)] = t
+        keep = [int(b) for b in t if 0 <= b < B]
+        valid_tables.append(keep)
+        valid_lens.append(lens[r] - bs * len(holes[r]))
+    q = torch.randn((2, hq, 128), generator=torch.Generator("cuda").manual_seed(5),
+                    device="cuda").to(torch.bfloat16)
+    max_seq = max(lens)
+    ws = torch.empty(fk.flowkv_decode_attention_workspace(2, hq, 128, max_seq, 64),
+                     dtype=torch.uint8, device="cuda")
+    out = torch.empty((2, hq, 128), dtype=torch.float32, device="cuda")
+    scale = 1.0 / np.sqrt(128)
+    fk.flowkv_decode_attention(pool, layer, q, torch.as_tensor(tab, device="cuda"),
+                               torch.as_tensor(np.asarray(lens, np.int32), device="cuda"),
+                               max_seq, scale, out, ws, 64)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.float64)
+    used = np.array(sorted({b for t in valid_tables for b in t}), dtype=np.int64)
+    host = download_blocks(pool, used)
+    lut = {int(b): i for i, b in enumerate(used)}
+    want = decode_attention(host, bf16_to_f64(q), [[lut[b] for b in t] for t in valid_tables],
+                            valid_lens, layer, geom.kv_heads, geom.head_dim, scale)
+    vmax = max(float(t.abs().max()) for t in pool.tensors)
+    err = np.abs(got - want).max()
+    assert np.all(np.isfinite(got))
+    assert err <= 2e-4 * vmax + 1e-6, err
