@@ -18,6 +18,10 @@ What it computes, each piece written from the paper's description:
 * :mod:`oracle.alloc`   -- the segment-based, contiguity-aware block allocator
   of section 3.3 (best-fit over free segments, merge on free), plus the two
   naive free-list policies used to build fragmented tables.
+* :mod:`oracle.attention` -- decode attention over a paged pool in either
+  layout (the PagedAttention consumer section 3.3 adapts), float64.
+* :mod:`oracle.scheduler` -- the Load-Aware Scheduler's evaluation and
+  routing (section 3.4, Algorithm 1), float64, term by term.
 
 Parity status of each function is stated in its module header.
 """
