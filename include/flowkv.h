@@ -292,6 +292,106 @@ int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer, const void* 
                             float* out_dev, void* workspace_dev, int64_t workspace_bytes,
                             void* hip_stream);
 
+/* ---- load-aware scheduler (section 3.4; Appendix A, Algorithm 1) ------------
+   Host only.  Each node reports a status vector S_i of 12 indicators, in
+   Algorithm 1's order:
+     0 L_r^p  1 L_w^p  2 L_sw^p  3 L_se^p   running, waiting, swapped and sending
+     4 L_r^d  5 L_w^d  6 L_sw^d  7 L_se^d   queue lengths, prefill then decode
+     8 T_b    9 KV_u  10 G_u    11 MB_u     token budget, KV-cache, GPU and
+                                            memory-bandwidth utilisation
+   The scheduler keeps a sliding window of samples per node; an evaluation
+   takes the window mean of each indicator divided by its scale, forms
+       C_i^p = w_p . (L_r^p, L_w^p, L_sw^p, L_se^p, T_b, KV_u, G_u, MB_u)
+       C_i^d = w_d . (L_r^d, L_w^d, L_sw^d, L_se^d, T_b, KV_u, G_u, MB_u)
+   (term by term in that order), averages C_i^p over the prefill-role nodes
+   and C_i^d over the decode-role nodes (0 for a role with no node), and
+   picks the scenario: normal when |C^p| <= eps_p_low and |C^d| <= eps_d_low;
+   imbalanced when both are within the high thresholds; extreme otherwise.
+   Readings of what Algorithm 1 leaves open:
+     - idle nodes (imbalanced) are the nodes of the less loaded role whose
+       own-role score is below idle_threshold; they are to take the busier
+       role, the one with the larger C / eps_low;
+     - extreme load asks for one more node of each role whose |C| exceeds
+       its high threshold once the scenario has lasted scale_after
+       consecutive evaluations (the count restarts after each scale request
+       and after any other scenario);
+     - routing (flowkv_sched_route) takes the prefill node with the least
+       (queued tokens + prompt tokens not in its prefix cache) / prefill
+       rate, then the decode node with room for the KV bytes and the least
+       latency + bytes x seconds-per-byte from that prefill node; ties go
+       to the lower index.
+   All arithmetic is IEEE double in the order stated, so results are exact
+   functions of the inputs.  Handles are not thread-safe. */
+
+#define FLOWKV_SCHED_INDICATORS 12
+#define FLOWKV_SCHED_TERMS 8
+#define FLOWKV_SCHED_MAX_WINDOW 4096
+
+enum { FLOWKV_ROLE_PREFILL = 0, FLOWKV_ROLE_DECODE = 1 };
+enum {
+  FLOWKV_SCENARIO_NORMAL = 0,
+  FLOWKV_SCENARIO_IMBALANCED = 1,
+  FLOWKV_SCENARIO_EXTREME = 2
+};
+
+typedef struct flowkv_sched_params {
+  int32_t window;       /* samples in the sliding window, 1..FLOWKV_SCHED_MAX_WINDOW */
+  int32_t scale_after;  /* consecutive extreme evaluations before a scale request, >= 1 */
+  double scale[FLOWKV_SCHED_INDICATORS];  /* normalisation divisors, > 0 */
+  double w_prefill[FLOWKV_SCHED_TERMS];   /* w_r, w_w, w_sw, w_se, w_t, w_kv, w_g, w_mb */
+  double w_decode[FLOWKV_SCHED_TERMS];
+  double eps_p_low, eps_d_low;            /* > 0 */
+  double eps_p_high, eps_d_high;          /* >= the low thresholds */
+  double idle_threshold;
+} flowkv_sched_params;
+
+typedef struct flowkv_sched_result {
+  int32_t scenario;       /* FLOWKV_SCENARIO_* */
+  int32_t n_idle;         /* idle node indices written (imbalanced), else 0 */
+  int32_t switch_to;      /* the role idle nodes take (imbalanced), else -1 */
+  int32_t scale_prefill;  /* 1: add a prefill node (extreme, persisted) */
+  int32_t scale_decode;   /* 1: add a decode node */
+  int32_t reserved;
+  double c_prefill;       /* C^p */
+  double c_decode;        /* C^d */
+} flowkv_sched_result;
+
+typedef struct flowkv_sched flowkv_sched; /* opaque, host memory only */
+
+/* New scheduler for n_nodes nodes (1..2^20) with initial roles[n_nodes]
+   (FLOWKV_ROLE_*).  The parameters are copied.  EINVAL for bad parameters,
+   ENOSPC if host memory runs out. */
+int flowkv_sched_create(const flowkv_sched_params* params, int32_t n_nodes,
+                        const int32_t* roles, flowkv_sched** out);
+void flowkv_sched_destroy(flowkv_sched* s);
+
+/* Change one node's role (a hybrid node switching, or a new node's role). */
+int flowkv_sched_set_role(flowkv_sched* s, int32_t node, int32_t role);
+
+/* One sample of every node's status: status[n_nodes x 12], row-major. */
+int flowkv_sched_observe(flowkv_sched* s, const double* status);
+
+/* One evaluation of Algorithm 1 over the samples in the window.  Writes
+   *res; idle node indices, ascending, to idle_nodes[0 .. res->n_idle)
+   (room for n_nodes; may be NULL only if the caller ignores them: then
+   n_idle is still set); node_scores[n_nodes x 2] = (C_i^p, C_i^d) if not
+   NULL.  EINVAL before the first observation. */
+int flowkv_sched_evaluate(flowkv_sched* s, flowkv_sched_result* res, int32_t* idle_nodes,
+                          double* node_scores);
+
+/* Routing of one request (normal load; the same rule serves the other
+   scenarios).  Per node i (all arrays n_nodes long; only the current role
+   is looked at): prefix_hit[i] prompt tokens already cached on i,
+   queued_tokens[i] prefill tokens waiting on i, prefill_rate[i] tokens per
+   second (nodes with rate <= 0 are skipped), free_bytes[i] KV bytes the node
+   can receive; xfer_sec_per_byte and xfer_latency are n_nodes x n_nodes,
+   row = sender.  Writes the chosen nodes, -1 where none qualifies. */
+int flowkv_sched_route(const flowkv_sched* s, int64_t prompt_tokens, const int64_t* prefix_hit,
+                       const int64_t* queued_tokens, const double* prefill_rate,
+                       int64_t kv_bytes, const double* xfer_sec_per_byte,
+                       const double* xfer_latency, const int64_t* free_bytes,
+                       int32_t* prefill_node, int32_t* decode_node);
+
 /* ---- diagnostics ------------------------------------------------------------ */
 
 /* Static name of a status code. */

@@ -1,7 +1,7 @@
 """Build the native library ``libflowkv.so`` in-tree for gfx950.
 
 ``python -m paper_2504_03775_amd.build`` compiles the host C++ (allocator,
-planner, status) with g++ and the HIP translation unit (kernel + launcher)
+planner, scheduler, status) with g++ and the HIP translation unit (kernel + launcher)
 with hipcc, then links them into ``paper_2504_03775_amd/libflowkv.so``.
 """
 
@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libflowkv.so")
 
-HOST_SOURCES = ["flowkv_status.cpp", "flowkv_alloc.cpp", "flowkv_plan.cpp"]
+HOST_SOURCES = ["flowkv_status.cpp", "flowkv_alloc.cpp", "flowkv_plan.cpp", "flowkv_sched.cpp"]
 HIP_SOURCES = ["flowkv_transfer.hip", "flowkv_attention.hip"]
 
 ARCH = "gfx950"

@@ -57,8 +57,24 @@ class flowkv_launch_config(ctypes.Structure):
                 ("grid", ctypes.c_int32), ("cache", ctypes.c_int32), ("order", ctypes.c_int32)]
 
 
+class flowkv_sched_params(ctypes.Structure):
+    _fields_ = [("window", ctypes.c_int32), ("scale_after", ctypes.c_int32),
+                ("scale", ctypes.c_double * 12), ("w_prefill", ctypes.c_double * 8),
+                ("w_decode", ctypes.c_double * 8), ("eps_p_low", ctypes.c_double),
+                ("eps_d_low", ctypes.c_double), ("eps_p_high", ctypes.c_double),
+                ("eps_d_high", ctypes.c_double), ("idle_threshold", ctypes.c_double)]
+
+
+class flowkv_sched_result(ctypes.Structure):
+    _fields_ = [("scenario", ctypes.c_int32), ("n_idle", ctypes.c_int32),
+                ("switch_to", ctypes.c_int32), ("scale_prefill", ctypes.c_int32),
+                ("scale_decode", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("c_prefill", ctypes.c_double), ("c_decode", ctypes.c_double)]
+
+
 _I32P = ctypes.POINTER(ctypes.c_int32)
 _I64P = ctypes.POINTER(ctypes.c_int64)
+_F64P = ctypes.POINTER(ctypes.c_double)
 _SEGP = ctypes.POINTER(flowkv_segment)
 _POOLP = ctypes.POINTER(flowkv_pool)
 
@@ -99,6 +115,15 @@ SIGNATURES = {
                                                ctypes.c_void_p, ctypes.c_int32, ctypes.c_float,
                                                ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                                ctypes.c_int64, ctypes.c_void_p]),
+    "flowkv_sched_create": (ctypes.c_int, [ctypes.POINTER(flowkv_sched_params), ctypes.c_int32,
+                                           _I32P, ctypes.POINTER(ctypes.c_void_p)]),
+    "flowkv_sched_destroy": (None, [ctypes.c_void_p]),
+    "flowkv_sched_set_role": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32]),
+    "flowkv_sched_observe": (ctypes.c_int, [ctypes.c_void_p, _F64P]),
+    "flowkv_sched_evaluate": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(flowkv_sched_result),
+                                             _I32P, _F64P]),
+    "flowkv_sched_route": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, _I64P, _I64P, _F64P,
+                                          ctypes.c_int64, _F64P, _F64P, _I64P, _I32P, _I32P]),
     "flowkv_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "flowkv_last_error": (ctypes.c_char_p, []),
 }
@@ -213,6 +238,86 @@ class Allocator:
 
     def stats(self) -> dict:
         return flowkv_allocator_stats(self._h)
+
+
+# ---- load-aware scheduler ------------------------------------------------------
+
+ROLE_PREFILL, ROLE_DECODE = 0, 1
+SCENARIO_NORMAL, SCENARIO_IMBALANCED, SCENARIO_EXTREME = 0, 1, 2
+SCHED_INDICATORS = 12
+
+
+def sched_params(window: int, scale, w_prefill, w_decode, eps_p_low: float, eps_d_low: float,
+                 eps_p_high: float, eps_d_high: float, idle_threshold: float,
+                 scale_after: int) -> flowkv_sched_params:
+    p = flowkv_sched_params()
+    p.window, p.scale_after = window, scale_after
+    p.scale[:] = [float(x) for x in scale]
+    p.w_prefill[:] = [float(x) for x in w_prefill]
+    p.w_decode[:] = [float(x) for x in w_decode]
+    p.eps_p_low, p.eps_d_low = eps_p_low, eps_d_low
+    p.eps_p_high, p.eps_d_high = eps_p_high, eps_d_high
+    p.idle_threshold = idle_threshold
+    return p
+
+
+class Scheduler:
+    """Owner of one flowkv_sched handle (Algorithm 1 of the paper)."""
+
+    def __init__(self, params: flowkv_sched_params, roles):
+        r = _i32(roles)
+        self.n = int(r.size)
+        h = ctypes.c_void_p()
+        _check(_lib.flowkv_sched_create(ctypes.byref(params), self.n, _ptr(r), ctypes.byref(h)),
+               "flowkv_sched_create")
+        self._h = h.value
+        self._destroy = _lib.flowkv_sched_destroy  # kept: module globals may be gone at exit
+        self._idle = np.empty(self.n, dtype=np.int32)
+        self._scores = np.empty((self.n, 2), dtype=np.float64)
+
+    def __del__(self):
+        h, self._h = getattr(self, "_h", None), None
+        if h:
+            self._destroy(h)
+
+    def set_role(self, node: int, role: int) -> None:
+        _check(_lib.flowkv_sched_set_role(self._h, node, role), "flowkv_sched_set_role")
+
+    def observe(self, status) -> None:
+        st = np.ascontiguousarray(np.asarray(status, dtype=np.float64))
+        if st.shape != (self.n, SCHED_INDICATORS):
+            raise ValueError(f"status must be ({self.n}, {SCHED_INDICATORS})")
+        _check(_lib.flowkv_sched_observe(self._h, st.ctypes.data_as(_F64P)),
+               "flowkv_sched_observe")
+
+    def evaluate(self):
+        """Returns (result struct, idle node array, (n, 2) array of C_i^p, C_i^d)."""
+        r = flowkv_sched_result()
+        _check(_lib.flowkv_sched_evaluate(self._h, ctypes.byref(r), _ptr(self._idle),
+                                          self._scores.ctypes.data_as(_F64P)),
+               "flowkv_sched_evaluate")
+        return r, self._idle[: r.n_idle].copy(), self._scores.copy()
+
+    def route(self, prompt_tokens: int, prefix_hit, queued_tokens, prefill_rate, kv_bytes: int,
+              xfer_sec_per_byte, xfer_latency, free_bytes):
+        """(prefill node, decode node) for one request; -1 where none qualifies."""
+        n = self.n
+        hit = np.ascontiguousarray(np.asarray(prefix_hit, dtype=np.int64))
+        q = np.ascontiguousarray(np.asarray(queued_tokens, dtype=np.int64))
+        rate = np.ascontiguousarray(np.asarray(prefill_rate, dtype=np.float64))
+        spb = np.ascontiguousarray(np.asarray(xfer_sec_per_byte, dtype=np.float64))
+        lat = np.ascontiguousarray(np.asarray(xfer_latency, dtype=np.float64))
+        free = np.ascontiguousarray(np.asarray(free_bytes, dtype=np.int64))
+        if hit.shape != (n,) or q.shape != (n,) or rate.shape != (n,) or free.shape != (n,) \
+                or spb.shape != (n, n) or lat.shape != (n, n):
+            raise ValueError("routing arrays do not match the node count")
+        pn, dn = ctypes.c_int32(), ctypes.c_int32()
+        _check(_lib.flowkv_sched_route(self._h, prompt_tokens, _ptr(hit, _I64P), _ptr(q, _I64P),
+                                       rate.ctypes.data_as(_F64P), kv_bytes,
+                                       spb.ctypes.data_as(_F64P), lat.ctypes.data_as(_F64P),
+                                       _ptr(free, _I64P), ctypes.byref(pn), ctypes.byref(dn)),
+               "flowkv_sched_route")
+        return pn.value, dn.value
 
 
 # ---- planner -----------------------------------------------------------------

@@ -1,4 +1,4 @@
-// Host-side stress driver for the allocator and planner of libflowkv, built
+// Host-side stress driver for the allocator, planner and scheduler of libflowkv, built
 // with AddressSanitizer and UndefinedBehaviorSanitizer by
 // tests/test_host_sanitizers.py (CPU only).
 //
@@ -211,6 +211,105 @@ void bad_arguments() {
   CHECK(flowkv_last_error() != nullptr);
 }
 
+// Load-aware scheduler: random parameters, status streams and role changes;
+// after every evaluation the result must be well formed (scenario in range,
+// idle nodes ascending, in range and of the role that is not asked for, the
+// node scores finite) and every route must name nodes of the right role.
+void sched_stream(uint64_t seed) {
+  std::mt19937_64 rng(seed);
+  std::uniform_real_distribution<double> u01(0.0, 1.0);
+  flowkv_sched_params p{};
+  p.window = 1 + int32_t(rng() % 8);
+  p.scale_after = 1 + int32_t(rng() % 3);
+  for (double& x : p.scale) x = 0.5 + 8.0 * u01(rng);
+  for (double& x : p.w_prefill) x = u01(rng);
+  for (double& x : p.w_decode) x = u01(rng);
+  p.eps_p_low = 0.1 + u01(rng);
+  p.eps_d_low = 0.1 + u01(rng);
+  p.eps_p_high = p.eps_p_low * (1.0 + 2.0 * u01(rng));
+  p.eps_d_high = p.eps_d_low * (1.0 + 2.0 * u01(rng));
+  p.idle_threshold = 0.5 * u01(rng);
+  const int32_t n = 1 + int32_t(rng() % 24);
+  std::vector<int32_t> roles(n);
+  for (auto& r : roles) r = int32_t(rng() % 2);
+  flowkv_sched* s = nullptr;
+  CHECK(flowkv_sched_create(&p, n, roles.data(), &s) == FLOWKV_OK && s);
+  flowkv_sched_result res{};
+  std::vector<int32_t> idle(n, -7);
+  std::vector<double> scores(2 * size_t(n));
+  CHECK(flowkv_sched_evaluate(s, &res, idle.data(), scores.data()) == FLOWKV_EINVAL);
+  std::vector<double> st(size_t(n) * FLOWKV_SCHED_INDICATORS);
+  double level = 0.1 + 2.0 * u01(rng);
+  for (int step = 0; step < 80; ++step) {
+    level *= 0.7 + 0.7 * u01(rng);
+    for (double& x : st) x = level * 8.0 * u01(rng);
+    CHECK(flowkv_sched_observe(s, st.data()) == FLOWKV_OK);
+    if (rng() % 8 == 0) {
+      const int32_t i = int32_t(rng() % n), role = int32_t(rng() % 2);
+      CHECK(flowkv_sched_set_role(s, i, role) == FLOWKV_OK);
+      roles[i] = role;
+    }
+    CHECK(flowkv_sched_evaluate(s, &res, idle.data(), scores.data()) == FLOWKV_OK);
+    CHECK(res.scenario >= FLOWKV_SCENARIO_NORMAL && res.scenario <= FLOWKV_SCENARIO_EXTREME);
+    CHECK(res.n_idle >= 0 && res.n_idle <= n);
+    if (res.scenario != FLOWKV_SCENARIO_IMBALANCED) CHECK(res.n_idle == 0 && res.switch_to == -1);
+    for (int32_t k = 0; k < res.n_idle; ++k) {
+      CHECK(idle[k] >= 0 && idle[k] < n && roles[idle[k]] != res.switch_to);
+      if (k) CHECK(idle[k] > idle[k - 1]);
+    }
+    for (double x : scores) CHECK(x == x && x >= 0.0);
+    // evaluating without the optional outputs gives the same result
+    flowkv_sched_result again{};
+    CHECK(flowkv_sched_observe(s, st.data()) == FLOWKV_OK);
+    CHECK(flowkv_sched_evaluate(s, &again, nullptr, nullptr) == FLOWKV_OK);
+    CHECK(again.n_idle >= 0 && again.n_idle <= n);
+  }
+  std::vector<int64_t> hit(n), queued(n), free_b(n);
+  std::vector<double> rate(n), spb(size_t(n) * n), lat(size_t(n) * n);
+  for (int k = 0; k < 200; ++k) {
+    const int64_t prompt = int64_t(rng() % 30000), kv = int64_t(rng() % (int64_t(1) << 33));
+    for (int32_t i = 0; i < n; ++i) {
+      hit[i] = int64_t(rng() % 40000);
+      queued[i] = int64_t(rng() % 100000);
+      rate[i] = (rng() % 4) ? 1000.0 + 10000.0 * u01(rng) : 0.0;
+      free_b[i] = (rng() % 3) ? kv + int64_t(rng() % 1000) : kv - 1;
+    }
+    for (double& x : spb) x = 1e-10 + 1e-9 * u01(rng);
+    for (double& x : lat) x = 1e-3 * u01(rng);
+    int32_t pn = -5, dn = -5;
+    CHECK(flowkv_sched_route(s, prompt, hit.data(), queued.data(), rate.data(), kv, spb.data(),
+                             lat.data(), free_b.data(), &pn, &dn) == FLOWKV_OK);
+    CHECK(pn == -1 || (pn >= 0 && pn < n && roles[pn] == FLOWKV_ROLE_PREFILL && rate[pn] > 0));
+    if (pn < 0) CHECK(dn == -1);
+    CHECK(dn == -1 || (dn >= 0 && dn < n && roles[dn] == FLOWKV_ROLE_DECODE && free_b[dn] >= kv));
+  }
+  // bad arguments
+  int32_t pn, dn;
+  CHECK(flowkv_sched_route(s, -1, hit.data(), queued.data(), rate.data(), 1, spb.data(),
+                           lat.data(), free_b.data(), &pn, &dn) == FLOWKV_EINVAL);
+  CHECK(flowkv_sched_route(s, 1, nullptr, queued.data(), rate.data(), 1, spb.data(), lat.data(),
+                           free_b.data(), &pn, &dn) == FLOWKV_EINVAL);
+  CHECK(flowkv_sched_set_role(s, n, 0) == FLOWKV_ERANGE);
+  CHECK(flowkv_sched_set_role(s, -1, 0) == FLOWKV_ERANGE);
+  CHECK(flowkv_sched_set_role(s, 0, 3) == FLOWKV_EINVAL);
+  CHECK(flowkv_sched_set_role(nullptr, 0, 0) == FLOWKV_EINVAL);
+  CHECK(flowkv_sched_observe(s, nullptr) == FLOWKV_EINVAL);
+  CHECK(flowkv_sched_evaluate(s, nullptr, nullptr, nullptr) == FLOWKV_EINVAL);
+  flowkv_sched_destroy(s);
+  flowkv_sched_destroy(nullptr);
+  flowkv_sched* t = nullptr;
+  CHECK(flowkv_sched_create(nullptr, 1, roles.data(), &t) == FLOWKV_EINVAL && !t);
+  CHECK(flowkv_sched_create(&p, 0, roles.data(), &t) == FLOWKV_EINVAL && !t);
+  flowkv_sched_params q = p;
+  q.window = FLOWKV_SCHED_MAX_WINDOW + 1;
+  CHECK(flowkv_sched_create(&q, 1, roles.data(), &t) == FLOWKV_EINVAL && !t);
+  q = p;
+  q.eps_d_high = q.eps_d_low / 2;
+  CHECK(flowkv_sched_create(&q, 1, roles.data(), &t) == FLOWKV_EINVAL && !t);
+  int32_t bad_role = 9;
+  CHECK(flowkv_sched_create(&p, 1, &bad_role, &t) == FLOWKV_EINVAL && !t);
+}
+
 }  // namespace
 
 int main(int argc, char** argv) {
@@ -219,6 +318,7 @@ int main(int argc, char** argv) {
   for (int r = 0; r < rounds; ++r) {
     for (int policy = 0; policy < 3; ++policy) allocator_stream(policy, uint64_t(r) * 7 + policy);
     plan_cases(uint64_t(r) * 13 + 5);
+    sched_stream(uint64_t(r) * 17 + 3);
   }
   std::printf("host_check: %d rounds ok\n", rounds);
   return 0;

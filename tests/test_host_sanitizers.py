@@ -15,7 +15,7 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2504_03775_amd", "csrc")
-HOST_SOURCES = ["flowkv_status.cpp", "flowkv_alloc.cpp", "flowkv_plan.cpp"]
+HOST_SOURCES = ["flowkv_status.cpp", "flowkv_alloc.cpp", "flowkv_plan.cpp", "flowkv_sched.cpp"]
 
 
 @pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not available")
