@@ -68,9 +68,11 @@ WORKLOADS = {
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--op", choices=["transfer", "attention"], default="transfer",
+    ap.add_argument("--op", choices=["transfer", "attention", "schedule"], default="transfer",
                     help="transfer: the KV transfer hot path (default); attention: one decode "
-                         "step of paged attention over the receiver pool of the batch workload")
+                         "step of paged attention over the receiver pool of the batch workload; "
+                         "schedule: the load-aware scheduler (host) at 1,024 nodes, and the "
+                         "cluster model's three load mixes with fixed and load-aware roles")
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="8b")
@@ -209,6 +211,92 @@ def bench_attention(args):
     print(json.dumps(line), flush=True)
 
 
+def bench_schedule(args):
+    """Load-aware scheduler (section 3.4, Algorithm 1), host code: evaluations
+    per second at 1,024 nodes (512 prefill, 512 decode, window 8), routing
+    calls per second, and the seeded cluster model's outcomes with fixed and
+    load-aware roles.  No device kernel runs in this mode."""
+    import numpy as np
+
+    from paper_2504_03775_amd import flowkv as fk
+    from workloads.cluster_sim import (STATUS_SCALE, Cluster, ClusterConfig, NativeScheduler,
+                                       Workload)
+
+    n, window = 1024, 8
+    w = [0.25, 0.25, 0.125, 0.125, 0.0625, 0.0625, 0.0625, 0.0625]
+    pargs = (window, STATUS_SCALE, w, w, 0.5, 0.5, 1.0, 1.0, 0.1, 3)
+    roles = [i % 2 for i in range(n)]
+    rng = np.random.default_rng(0)
+    samples = rng.uniform(0, 4, size=(64, n, 12))
+    nat = fk.Scheduler(fk.sched_params(*pargs), roles)
+
+    def evals(sched, k):
+        for i in range(k):
+            sched.observe(samples[i % len(samples)])
+            sched.evaluate()
+
+    evals(nat, args.warmup)
+    t0 = time.perf_counter()
+    evals(nat, args.steps)
+    t_eval = (time.perf_counter() - t0) / args.steps
+    zeros = np.zeros(n, dtype=np.int64)
+    queued = rng.integers(0, 100_000, n)
+    rate = np.where(np.asarray(roles) == 0, 40_000.0, 0.0)
+    spb = np.full((n, n), 2e-11)
+    lat = np.full((n, n), 5e-5)
+    free = np.full(n, 1 << 40, dtype=np.int64)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        nat.route(8000, zeros, queued, rate, 8000 * 131072, spb, lat, free)
+    t_route = (time.perf_counter() - t0) / args.steps
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle.scheduler import Params, RefScheduler
+        ref = RefScheduler(Params(window, STATUS_SCALE, w, w, 0.5, 0.5, 1.0, 1.0, 0.1, 3), roles)
+        k = 3
+        as_lists = [s_.tolist() for s_ in samples[:k]]
+        t0 = time.perf_counter()
+        for i in range(k):
+            ref.observe(as_lists[i])
+            ref.evaluate()
+        t_ref = (time.perf_counter() - t0) / k
+        cpu = {"value": round(1.0 / t_ref, 2), "unit": "evaluations/s", "cores": 1,
+               "kind": "oracle", "sample": f"{k} evaluations at {n} nodes, window {window}, "
+                                          "pure Python"}
+
+    mixes = {"balanced": Workload(6.0, 400, [1000, 5000, 10000], [256], seed=1),
+             "prefill-heavy": Workload(5.0, 300, [12000, 16000, 20000], [32], seed=2),
+             "decode-heavy": Workload(30.0, 600, [500, 1000], [1024], seed=3)}
+    sim = {}
+    for name, wl in mixes.items():
+        row = {}
+        for label, sw in (("fixed", False), ("load_aware", True)):
+            r4 = [0, 0, 1, 1]
+            c = Cluster(ClusterConfig(roles=r4, switching=sw),
+                        NativeScheduler(fk, fk.sched_params(4, *pargs[1:]), r4))
+            out = c.run(wl)
+            row[label] = {k_: (round(v, 4) if isinstance(v, float) else v)
+                          for k_, v in out.items()
+                          if k_ in ("requests_per_s", "ttft_mean_s", "e2e_mean_s",
+                                    "role_switches", "scenario_ticks")}
+        sim[name] = row
+    line = {
+        "metric": "load-aware scheduler evaluations per second (1,024 nodes, window 8)",
+        "value": round(1.0 / t_eval, 1), "unit": "evaluations/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t_eval * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": "load-aware-scheduler-1024-nodes", "nodes": n, "window": window,
+                   "prefill_nodes": n // 2, "decode_nodes": n // 2},
+        "route_us": round(t_route * 1e6, 2),
+        "roofline": None,
+        "cpu_baseline": cpu,
+        "context": {"cluster_model_2p2d": sim},
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -217,6 +305,9 @@ def main():
         sys.exit(2)
     if args.op == "attention":
         bench_attention(args)
+        return
+    if args.op == "schedule":
+        bench_schedule(args)
         return
 
     import numpy as np

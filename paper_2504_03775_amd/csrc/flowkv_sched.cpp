@@ -110,13 +110,14 @@ extern "C" int flowkv_sched_evaluate(flowkv_sched* s, flowkv_sched_result* res,
   // per node: window means (oldest sample first), normalised, then the two
   // weighted sums term by term
   for (int32_t i = 0; i < s->n; ++i) {
-    double norm[kInd];
-    for (int k = 0; k < kInd; ++k) {
-      double acc = 0.0;
-      for (int32_t j = 0; j < s->count; ++j)
-        acc += s->ring[(size_t(i) * W + (s->head + j) % W) * kInd + k];
-      norm[k] = acc / double(s->count) / p.scale[k];
+    double acc[kInd] = {};
+    const double* node = &s->ring[size_t(i) * W * kInd];
+    for (int32_t j = 0, slot = s->head; j < s->count; ++j, slot = slot + 1 == W ? 0 : slot + 1) {
+      const double* x = node + size_t(slot) * kInd;
+      for (int k = 0; k < kInd; ++k) acc[k] += x[k];
     }
+    double norm[kInd];
+    for (int k = 0; k < kInd; ++k) norm[k] = acc[k] / double(s->count) / p.scale[k];
     double cp = 0.0, cd = 0.0;
     for (int t = 0; t < kTerms; ++t) cp += p.w_prefill[t] * norm[kPrefillTerms[t]];
     for (int t = 0; t < kTerms; ++t) cd += p.w_decode[t] * norm[kDecodeTerms[t]];
