@@ -48,6 +48,11 @@ HBM_PEAK_GBPS = 8000.0
 METRIC = "effective KV transfer GB/s (% of HBM peak); ms per 13k-token request transfer"
 KERNEL_SRC = os.path.join(ROOT, "paper_2504_03775_amd", "csrc", "flowkv_transfer.hip")
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "kv_segment_copy_llama3-8b-13k_pmc.txt")
+ATTN_SRC = os.path.join(ROOT, "paper_2504_03775_amd", "csrc", "flowkv_attention.hip")
+ATTN_PMC_SUMMARY = {
+    "batch": os.path.join(ROOT, "profiles", "decode_attn_llama3-8b-batch32_pmc.txt"),
+    "70b": os.path.join(ROOT, "profiles", "decode_attn_llama3-70b-tp8-share_pmc.txt"),
+}
 
 WORKLOADS = {
     # name: (recipe, args, description)
@@ -105,19 +110,19 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_hash() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+def kernel_hash(src: str = KERNEL_SRC) -> str:
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
 
 
-def traffic_from_profile():
+def traffic_from_profile(summary: str = PMC_SUMMARY, src: str = KERNEL_SRC):
     """HBM bytes per launch from the committed counter summary, scaled by the
     plain-copy calibration recorded with it; None if absent or if the kernel
     source changed since the counters were taken."""
-    if not os.path.exists(PMC_SUMMARY):
+    if not summary or not os.path.exists(summary):
         return None
-    text = open(PMC_SUMMARY).read()
+    text = open(summary).read()
     m = re.search(r"kernel_source_sha256_16:\s*(\w+)", text)
-    if not m or m.group(1) != kernel_hash():
+    if not m or m.group(1) != kernel_hash(src):
         return None
     t = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
     return float(t.group(1)) if t else None
@@ -186,6 +191,32 @@ def bench_attention(args):
     elapsed = time.perf_counter() - t0
     gc.enable()
     ms = statistics.fmean(a.elapsed_time(b) for a, b in evs)
+
+    context = {}
+    if not args.no_context:
+        # plain contiguous device-to-device copy: context, and the kernel that
+        # scales HBM counters taken from this process
+        nbytes = int(args.calibrate_copy_gib * (1 << 30))
+        a_ = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        b_ = torch.empty_like(a_)
+        for _ in range(3):
+            b_.copy_(a_)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(10):
+            b_.copy_(a_)
+        e1.record()
+        torch.cuda.synchronize()
+        context = {"contiguous_copy_gbps": round(2 * nbytes / (e0.elapsed_time(e1) / 10 * 1e-3)
+                                                 / 1e9, 1),
+                   "contiguous_copy_bytes": nbytes}
+        del a_, b_
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = attention_cpu_baseline(pool, geom, layer, q, wl, lens, scale, np, torch)
+
     kv_bytes = int(lens.sum()) * 2 * geom.kv_heads * geom.head_dim * 2
     split = args.split or fk.flowkv_decode_attention_split(len(lens), max_seq)
     # workspace: written by pass 1 and read by pass 2, for the splits that exist
@@ -206,9 +237,46 @@ def bench_attention(args):
                    "layout": f"{args.layout}-major", "layer": layer, "split_tokens": split},
         "kernel_ms_avg": round(ms, 4),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None},
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic_from_profile(ATTN_PMC_SUMMARY.get(args.attn_workload)
+                                                     if args.layout == "block" and not args.split
+                                                     else None, ATTN_SRC)},
+        "cpu_baseline": cpu,
+        "context": context,
     }
     print(json.dumps(line), flush=True)
+
+
+def attention_cpu_baseline(pool, geom, layer, q, wl, lens, scale, np, torch):
+    """The float64 oracle on the host, on a bounded sample: the workload's
+    shortest request (its blocks downloaded to a compact host pool), timed
+    once; reported as K/V bytes read per second."""
+    import oracle
+    from oracle.attention import decode_attention
+
+    r = int(np.argmin(lens))
+    ids = np.asarray(wl.tables[r][1], dtype=np.int64)
+    T = int(lens[r])
+    idx = torch.as_tensor(ids, device=pool.device)
+    slot = pool.kv_heads * pool.head_dim * pool.elem_bytes
+    hp = oracle.HostPool.zeros(pool.layout, pool.num_layers, len(ids), pool.block_size, slot)
+    if pool.layout == 1:    # block-major: one tensor, rows are blocks
+        hp.buffers[0][:] = pool.tensors[0].index_select(0, idx).view(torch.uint8).cpu() \
+            .numpy().reshape(-1)
+    else:                   # layer-major: per layer (2, B, ...)
+        for l_, t in enumerate(pool.tensors):
+            hp.buffers[l_][:] = t.index_select(1, idx).contiguous().view(torch.uint8).cpu() \
+                .numpy().reshape(-1)
+    qh = q[r:r + 1].float().cpu().numpy().astype(np.float64)
+    t0 = time.perf_counter()
+    decode_attention(hp, qh, [list(range(len(ids)))], [T], layer, geom.kv_heads,
+                     geom.head_dim, scale)
+    dt = time.perf_counter() - t0
+    kv = T * 2 * geom.kv_heads * geom.head_dim * 2
+    return {"value": round(kv / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"request {r} of the workload ({T} tokens, {kv} K/V bytes), one layer, "
+                      f"float64 numpy with a per-slot gather, one thread; "
+                      f"{os.cpu_count()} host cores visible"}
 
 
 def bench_schedule(args):
