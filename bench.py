@@ -114,13 +114,18 @@ def kernel_hash(src: str = KERNEL_SRC) -> str:
     return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
 
 
-def traffic_from_profile(summary: str = PMC_SUMMARY, src: str = KERNEL_SRC):
+def traffic_from_profile(summary: str = PMC_SUMMARY, src: str = KERNEL_SRC, split=None):
     """HBM bytes per launch from the committed counter summary, scaled by the
-    plain-copy calibration recorded with it; None if absent or if the kernel
-    source changed since the counters were taken."""
+    plain-copy calibration recorded with it; None if absent, if the kernel
+    source changed since the counters were taken, or (attention) if they were
+    taken at another split length."""
     if not summary or not os.path.exists(summary):
         return None
     text = open(summary).read()
+    if split is not None:
+        ms = re.search(r"split_tokens:\s*(\d+)", text)
+        if not ms or int(ms.group(1)) != split:
+            return None
     m = re.search(r"kernel_source_sha256_16:\s*(\w+)", text)
     if not m or m.group(1) != kernel_hash(src):
         return None
@@ -239,8 +244,8 @@ def bench_attention(args):
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic_from_profile(ATTN_PMC_SUMMARY.get(args.attn_workload)
-                                                     if args.layout == "block" and not args.split
-                                                     else None, ATTN_SRC)},
+                                                     if args.layout == "block" else None,
+                                                     ATTN_SRC, split)},
         "cpu_baseline": cpu,
         "context": context,
     }
