@@ -581,6 +581,28 @@ def main():
             torch.cuda.synchronize()
             context["per_chunk_copy_calls"] = calls
             context["per_chunk_copy_ms"] = round((time.perf_counter() - t_chunks) * 1e3, 2)
+            # one copy per aligned run (per run, layer and K/V in the layer-major
+            # layout): the call pattern of a per-run transfer API
+            segs_h = fk.flowkv_plan(S_all, D, src_blocks, dst_blocks)
+            torch.cuda.synchronize()
+            t_runs = time.perf_counter()
+            calls = 0
+            if layout == fk.LAYOUT_BLOCK_MAJOR:
+                for sg in segs_h:
+                    s0, d0, m = int(sg["src_block"]), int(sg["dst_block"]), int(sg["n_blocks"])
+                    dst.tensors[0][d0:d0 + m].copy_(src.tensors[0][s0:s0 + m])
+                    calls += 1
+            else:
+                for ts, td in zip(src.tensors, dst.tensors):
+                    for kv in range(2):
+                        for sg in segs_h:
+                            s0, d0 = int(sg["src_block"]), int(sg["dst_block"])
+                            m = int(sg["n_blocks"])
+                            td[kv, d0:d0 + m].copy_(ts[kv, s0:s0 + m])
+                            calls += 1
+            torch.cuda.synchronize()
+            context["per_run_copy_calls"] = calls
+            context["per_run_copy_ms"] = round((time.perf_counter() - t_runs) * 1e3, 3)
 
     # ---- CPU baseline: the oracle on the host ----------------------------------------
     cpu = None
@@ -608,11 +630,28 @@ def main():
             t_cpu += time.perf_counter() - t1
             reps += 1
         sample_bytes = k * geom.block_bytes
+        # the same oracle call per layer on a thread pool (numpy's copies
+        # release the interpreter lock): the host's cores together
+        from concurrent.futures import ThreadPoolExecutor
+        threads = min(16, os.cpu_count() or 1, geom.num_layers)
+        ids = np.arange(k)
+        with ThreadPoolExecutor(threads) as ex:
+            reps_m, t_m = 0, 0.0
+            while t_m < 5.0 and reps_m < 20:
+                t1 = time.perf_counter()
+                list(ex.map(lambda l: oracle.transfer_fast(h_src, h_dst, ids, ids, layers=[l]),
+                            range(geom.num_layers)))
+                t_m += time.perf_counter() - t1
+                reps_m += 1
         cpu = {"value": round(sample_bytes * reps / t_cpu / 1e9, 3), "unit": "GB/s", "cores": 1,
                "kind": "oracle",
                "sample": f"{k} of the workload's {n} blocks ({sample_bytes} B), repeated {reps}x, "
                          f"compact host pools of those blocks, numpy one thread; "
-                         f"{os.cpu_count()} host cores visible"}
+                         f"{os.cpu_count()} host cores visible",
+               "multi_thread": {"value": round(sample_bytes * reps_m / t_m / 1e9, 3),
+                                "cores": threads,
+                                "sample": f"the same, one oracle call per layer on {threads} "
+                                          f"threads, repeated {reps_m}x"}}
         del h_src, h_dst
 
     traffic = traffic_from_profile() if (single and args.layout == "block"
@@ -646,6 +685,8 @@ def main():
         ("ms_per_request" if single else "ms_per_plan_latency"): round(ms_latency, 4),
         "pct_of_hbm_peak": round(100 * achieved / HBM_PEAK_GBPS, 2),
         "kernel_ms_avg": round(kern_avg_ms, 4),
+        "kernel_ms_p10_p50_p90": [round(float(x), 4) for x in
+                                  np.percentile(np.asarray(kern_ms), [10, 50, 90])],
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic},
