@@ -8,24 +8,28 @@
 // layout through the request's block list.  Grouped KV heads: Hq query heads
 // share Hkv KV heads, query head h reading KV head h / (Hq / Hkv).
 //
-// Decode attention reads every cached K and V element once and does ~2
-// flops per byte: it is HBM-bound, so it runs on the vector units (no MFMA),
-// and the work per token is kept small enough that the loads stay the limit.
+// Decode attention reads every cached K and V element once and does about
+// G flops per byte (G = Hq / Hkv query heads per KV head): it is HBM-bound,
+// so it runs on the vector units (no MFMA), and the work per token is kept
+// small enough that the loads stay the limit.
 // Work split (flash-decoding style):
 //   pass 1: one workgroup per (KV head, token split, request).  A token's
 //           head vector (Dh bf16) is read by one 16-lane DPP row, Dh/16
 //           values per lane; the workgroup's 16 rows take the split's tokens
-//           round-robin, 4 tokens per row per step.
+//           round-robin, 4 tokens per row per step (with G = 8, two rows
+//           share each token, 4 query heads each).  The loads are
+//           branch-free, so their count per step is static.
 //           - q.k: bf16 pair dot products (v_dot2) on the raw bf16 values.
-//           - The kTok x G partial scores of a row are summed over its 16
-//             lanes by a transposed butterfly (row mirror, half mirror, two
-//             quad swaps): each step halves the values a lane holds, so the
-//             row ends with every (token, head) score owned by one lane
-//             (or replicated when there are fewer than 16).
+//           - The 4 x (heads per row) partial scores of a row are summed
+//             over its 16 lanes by a transposed butterfly (row mirror, half
+//             mirror, two quad swaps): each step halves the values a lane
+//             holds, so the row ends with every (token, head) score owned by
+//             one lane (or replicated when there are fewer than 16).
 //           - The owner lane runs the online softmax for its score: a
 //             running reference max per head, moved only when a score
-//             exceeds it by more than 2^kLazy (so weights stay <= 2^kLazy and
-//             the weighted sums are rarely rescaled).
+//             exceeds it by more than kLazy (log2 units), so unnormalised
+//             weights stay <= 2^kLazy and the weighted sums are rarely
+//             rescaled.
 //           - The weights and rescale factors go through a small LDS row
 //             buffer to all 16 lanes, which accumulate weight x V in float32.
 //           Rows merge through LDS and the workgroup writes its partial

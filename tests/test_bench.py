@@ -54,3 +54,38 @@ def test_bench_line_contract_on_tiny(layout):
     assert abs(rf["frac"] - rf["achieved"] / rf["peak"]) < 1e-3
     cb = j["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["cores"] >= 1 and cb["value"] > 0
+
+
+def test_schedule_line_contract_on_cpu():
+    """bench.py --op schedule runs on the host alone: one JSON line with the
+    scheduler's rate, the oracle beside it and the cluster model's mixes."""
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--op", "schedule",
+                        "--steps", "20", "--warmup", "2"],
+                       capture_output=True, text=True, timeout=600, cwd=ROOT)
+    assert r.returncode == 0, r.stderr[-2000:]
+    lines = [l for l in r.stdout.splitlines() if l.strip()]
+    assert len(lines) == 1
+    j = json.loads(lines[0])
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
+                "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config",
+                "roofline", "cpu_baseline", "context"):
+        assert key in j, key
+    assert j["value"] > 0 and j["roofline"] is None and j["dtype"] == "f64"
+    assert j["cpu_baseline"]["kind"] == "oracle" and j["cpu_baseline"]["value"] > 0
+    sim = j["context"]["cluster_model_2p2d"]
+    assert set(sim) == {"balanced", "prefill-heavy", "decode-heavy"}
+    dh = sim["decode-heavy"]
+    assert dh["load_aware"]["requests_per_s"] > dh["fixed"]["requests_per_s"]
+
+
+@pytest.mark.gpu
+def test_attention_line_contract():
+    j = run_bench("--op", "attention", "--attn-workload", "70b", "--steps", "3", "--warmup", "1",
+                  "--no-context", "--no-cpu-baseline")
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
+                "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config",
+                "roofline"):
+        assert key in j, key
+    assert j["config"]["kv_heads"] == 1 and j["config"]["q_heads"] == 8
+    assert j["config"]["split_tokens"] == 512 and j["value"] > 0
+    assert j["roofline"]["bound"] == "hbm"
