@@ -83,21 +83,21 @@ SIGNATURES = {
     "flowkv_allocator_create": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_uint64,
                                                ctypes.POINTER(ctypes.c_void_p)]),
     "flowkv_allocator_destroy": (None, [ctypes.c_void_p]),
-    "flowkv_alloc": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, _I32P]),
-    "flowkv_free": (ctypes.c_int, [ctypes.c_void_p, _I32P, ctypes.c_int32]),
-    "flowkv_mark_used": (ctypes.c_int, [ctypes.c_void_p, _I32P, ctypes.c_int32]),
+    "flowkv_alloc": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]),
+    "flowkv_free": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32]),
+    "flowkv_mark_used": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32]),
     "flowkv_allocator_stats": (ctypes.c_int, [ctypes.c_void_p,
                                               ctypes.POINTER(flowkv_alloc_stats)]),
-    "flowkv_plan": (ctypes.c_int, [_I32P, _I32P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
-                                   _SEGP, ctypes.c_int64, _I64P]),
-    "flowkv_plan_batch": (ctypes.c_int, [ctypes.c_int32, _I64P, _I32P, _I32P, ctypes.c_int32,
-                                         ctypes.c_int32, _SEGP, ctypes.c_int64, _I64P]),
+    "flowkv_plan": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                   ctypes.c_void_p, ctypes.c_int64, _I64P]),
+    "flowkv_plan_batch": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                         ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64, _I64P]),
     "flowkv_transfer": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_int64,
                                        ctypes.c_int64, ctypes.c_void_p]),
     "flowkv_transfer_ex": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_int64,
                                           ctypes.c_int64, ctypes.POINTER(flowkv_launch_config),
                                           ctypes.c_void_p]),
-    "flowkv_transfer_inline": (ctypes.c_int, [_POOLP, _POOLP, _SEGP, ctypes.c_int64,
+    "flowkv_transfer_inline": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_int64,
                                               ctypes.c_int64, ctypes.POINTER(flowkv_launch_config),
                                               ctypes.c_void_p]),
     "flowkv_transfer_layers": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_int64,
@@ -116,14 +116,14 @@ SIGNATURES = {
                                                ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                                ctypes.c_int64, ctypes.c_void_p]),
     "flowkv_sched_create": (ctypes.c_int, [ctypes.POINTER(flowkv_sched_params), ctypes.c_int32,
-                                           _I32P, ctypes.POINTER(ctypes.c_void_p)]),
+                                           ctypes.c_void_p, ctypes.POINTER(ctypes.c_void_p)]),
     "flowkv_sched_destroy": (None, [ctypes.c_void_p]),
     "flowkv_sched_set_role": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32]),
-    "flowkv_sched_observe": (ctypes.c_int, [ctypes.c_void_p, _F64P]),
+    "flowkv_sched_observe": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
     "flowkv_sched_evaluate": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(flowkv_sched_result),
-                                             _I32P, _F64P]),
-    "flowkv_sched_route": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, _I64P, _I64P, _F64P,
-                                          ctypes.c_int64, _F64P, _F64P, _I64P, _I32P, _I32P]),
+                                             ctypes.c_void_p, ctypes.c_void_p]),
+    "flowkv_sched_route": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, _I32P, _I32P]),
     "flowkv_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "flowkv_last_error": (ctypes.c_char_p, []),
 }
@@ -174,8 +174,11 @@ def _i32(a) -> np.ndarray:
     return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
 
 
-def _ptr(a: np.ndarray, t=_I32P):
-    return a.ctypes.data_as(t)
+def _ptr(a: np.ndarray, t=None) -> int:
+    """The array's address, for a c_void_p argument (a typed ctypes pointer
+    costs several microseconds per call to build, and the array interface
+    dictionary of a structured array as much)."""
+    return a.ctypes.data
 
 
 # ---- allocator ---------------------------------------------------------------
@@ -221,11 +224,12 @@ class Allocator:
         self.num_blocks = num_blocks
         self.policy = policy
         self._h = flowkv_allocator_create(num_blocks, policy, seed)
+        self._destroy = _lib.flowkv_allocator_destroy  # kept: module globals may be gone at exit
 
     def __del__(self):
         h, self._h = getattr(self, "_h", None), None
         if h:
-            flowkv_allocator_destroy(h)
+            self._destroy(h)
 
     def alloc(self, n: int) -> np.ndarray:
         return flowkv_alloc(self._h, n)
@@ -287,14 +291,14 @@ class Scheduler:
         st = np.ascontiguousarray(np.asarray(status, dtype=np.float64))
         if st.shape != (self.n, SCHED_INDICATORS):
             raise ValueError(f"status must be ({self.n}, {SCHED_INDICATORS})")
-        _check(_lib.flowkv_sched_observe(self._h, st.ctypes.data_as(_F64P)),
+        _check(_lib.flowkv_sched_observe(self._h, _ptr(st)),
                "flowkv_sched_observe")
 
     def evaluate(self):
         """Returns (result struct, idle node array, (n, 2) array of C_i^p, C_i^d)."""
         r = flowkv_sched_result()
         _check(_lib.flowkv_sched_evaluate(self._h, ctypes.byref(r), _ptr(self._idle),
-                                          self._scores.ctypes.data_as(_F64P)),
+                                          _ptr(self._scores)),
                "flowkv_sched_evaluate")
         return r, self._idle[: r.n_idle].copy(), self._scores.copy()
 
@@ -313,8 +317,8 @@ class Scheduler:
             raise ValueError("routing arrays do not match the node count")
         pn, dn = ctypes.c_int32(), ctypes.c_int32()
         _check(_lib.flowkv_sched_route(self._h, prompt_tokens, _ptr(hit, _I64P), _ptr(q, _I64P),
-                                       rate.ctypes.data_as(_F64P), kv_bytes,
-                                       spb.ctypes.data_as(_F64P), lat.ctypes.data_as(_F64P),
+                                       _ptr(rate), kv_bytes,
+                                       _ptr(spb), _ptr(lat),
                                        _ptr(free, _I64P), ctypes.byref(pn), ctypes.byref(dn)),
                "flowkv_sched_route")
         return pn.value, dn.value
@@ -330,7 +334,7 @@ def flowkv_plan(src_ids, dst_ids, src_pool_blocks: int, dst_pool_blocks: int) ->
     out = np.empty(max(s.size, 1), dtype=SEGMENT_DTYPE)
     n = ctypes.c_int64()
     _check(_lib.flowkv_plan(_ptr(s), _ptr(d), s.size, src_pool_blocks, dst_pool_blocks,
-                            out.ctypes.data_as(_SEGP), out.size, ctypes.byref(n)), "flowkv_plan")
+                            _ptr(out), out.size, ctypes.byref(n)), "flowkv_plan")
     return out[: n.value]
 
 
@@ -344,7 +348,7 @@ def flowkv_plan_batch(offsets, src_ids, dst_ids, src_pool_blocks: int,
     out = np.empty(max(s.size, 1), dtype=SEGMENT_DTYPE)
     n = ctypes.c_int64()
     _check(_lib.flowkv_plan_batch(off.size - 1, _ptr(off, _I64P), _ptr(s), _ptr(d),
-                                  src_pool_blocks, dst_pool_blocks, out.ctypes.data_as(_SEGP),
+                                  src_pool_blocks, dst_pool_blocks, _ptr(out),
                                   out.size, ctypes.byref(n)), "flowkv_plan_batch")
     return out[: n.value]
 
@@ -437,7 +441,7 @@ def flowkv_transfer_inline(src: KVPool, dst: KVPool, segs: np.ndarray, total_blo
     segs = np.ascontiguousarray(segs, dtype=SEGMENT_DTYPE)
     cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
     _check(_lib.flowkv_transfer_inline(ctypes.byref(src.desc), ctypes.byref(dst.desc),
-                                       segs.ctypes.data_as(_SEGP), len(segs), total_blocks,
+                                       _ptr(segs), len(segs), total_blocks,
                                        ctypes.byref(cfg), ctypes.c_void_p(_stream_handle(stream))),
            "flowkv_transfer_inline")
 
