@@ -26,3 +26,20 @@ def pytest_collection_modifyitems(config, items):
     for item in items:
         if "gpu" in item.keywords:
             item.add_marker(skip)
+
+
+@pytest.fixture(autouse=True)
+def _release_device_memory(request):
+    """After each GPU test, return the memory torch's caching allocator still
+    holds to the device: the full-size tests need most of the 288 GB, and a
+    pool an earlier test dropped must not count against them."""
+    yield
+    if "gpu" not in request.keywords:
+        return
+    import gc
+
+    import torch
+    if torch.cuda.is_available():
+        gc.collect()
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()

@@ -7,6 +7,8 @@ and the receiver's pre-image)."""
 
 from __future__ import annotations
 
+import gc
+
 import numpy as np
 import torch
 
@@ -109,6 +111,8 @@ def check_sampled(wl, wl_ref, sl, dl, max_blocks=1536, untouched_frac=0.01, max_
         assert np.array_equal(s1, s2) and np.array_equal(d1, d2)
     geom = wl.geom
     need = pool_bytes(geom, wl.src_pool_blocks) + pool_bytes(geom, wl.dst_pool_blocks)
+    gc.collect()
+    torch.cuda.empty_cache()
     free, _ = torch.cuda.mem_get_info()
     assert need < free, f"pools need {need / 2**30:.1f} GiB, {free / 2**30:.1f} GiB free"
     src = device_pool(geom, sl, wl.src_pool_blocks, 0)
