@@ -569,6 +569,11 @@ extern "C" int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer,
                 (long long)need);
   if (reinterpret_cast<uintptr_t>(q_dev) % 16)
     return fail(FLOWKV_EINVAL, "query not 16-byte aligned");
+  // the launch grids put requests and splits on dimensions limited to 65,535
+  const int64_t splits = (int64_t(max_seq_len) + split_tokens - 1) / split_tokens;
+  if (n_req > 65535 || splits > 65535)
+    return fail(FLOWKV_EINVAL, "%d requests, %lld splits: each must be at most 65535 per call",
+                n_req, (long long)splits);
   const bool lm = pool->layout == FLOWKV_LAYOUT_LAYER_MAJOR;
   const int nbase = lm ? pool->num_layers : 1;
   AttnArgs a{};

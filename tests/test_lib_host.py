@@ -307,3 +307,33 @@ def test_binding_shares_torchs_hip_runtime():
     """Device pointers and streams come from torch, so the library must bind
     to torch's HIP runtime: exactly one libamdhip64 may be mapped."""
     assert len(fk._hip_runtimes_loaded()) == 1
+
+
+# ---- decode attention argument checks (rejected before any device call) ------
+
+def attn(p, layer=0, q=1 << 12, n_req=1, hq=8, hkv=2, dh=128, tables=1 << 16, max_blocks=4,
+         lens=1 << 18, max_seq=64, scale=0.1, split=0, out=1 << 20, ws=1 << 24, ws_bytes=1 << 30):
+    return fk.lib().flowkv_decode_attention(
+        ctypes.byref(p), layer, ctypes.c_void_p(q), n_req, hq, hkv, dh, ctypes.c_void_p(tables),
+        max_blocks, ctypes.c_void_p(lens), max_seq, scale, split, ctypes.c_void_p(out),
+        ctypes.c_void_p(ws), ws_bytes, None)
+
+
+def test_attention_rejects_bad_arguments_without_touching_the_device():
+    chunk = 16 * 2 * 128 * 2                       # bs 16, 2 KV heads, head_dim 128, bf16
+    p = pool(L=2, B=8, chunk=chunk)
+    assert attn(p, n_req=0) == fk.OK              # nothing to do: no launch
+    cases = [
+        dict(layer=2), dict(layer=-1), dict(dh=96), dict(hq=6, hkv=4), dict(hq=32, hkv=2),
+        dict(split=1025), dict(split=-3), dict(scale=0.0), dict(scale=float("inf")),
+        dict(q=(1 << 12) + 8),                     # query not 16-byte aligned
+        dict(n_req=70000),                         # past the grid's 65,535 requests
+        dict(max_seq=70000, split=1),              # past the grid's 65,535 splits
+        dict(max_blocks=-1), dict(q=0), dict(ws=0),
+    ]
+    for c in cases:
+        assert attn(p, **c) == fk.EINVAL, c
+    assert attn(p, ws_bytes=16) == fk.ECAP
+    assert attn(pool(L=2, B=8, chunk=chunk + 16)) == fk.EINVAL    # chunk not bs x Hkv x Dh x 2
+    assert attn(pool(layout=7, L=2, B=8, chunk=chunk)) == fk.EINVAL
+    assert attn(pool(L=2, B=8, chunk=chunk, bases=(0,))) == fk.EINVAL   # NULL base
