@@ -1,9 +1,10 @@
 """ctypes binding to ``libflowkv.so`` (the C ABI in ``include/flowkv.h``).
 
-Argument marshalling only: every step -- allocation, alignment, the copy --
-runs in the native library.  PyTorch supplies device memory and streams.
-The functions carry the C names; ``Allocator`` and ``KVPool`` are thin owners
-of a handle and of a pool descriptor.
+Argument marshalling only: every step -- allocation, alignment, the copy,
+decode attention, the scheduler's evaluation and routing -- runs in the
+native library.  PyTorch supplies device memory and streams.  The functions
+carry the C names; ``Allocator``, ``Scheduler`` and ``KVPool`` are thin
+owners of a handle or of a pool descriptor.
 
 If the library is missing this module raises on import: there is no other
 code path.
@@ -490,6 +491,8 @@ def flowkv_decode_attention(pool: KVPool, layer: int, q, block_tables, seq_lens,
             raise ValueError("attention tensors: wrong dtype, layout or device")
     if tuple(out.shape) != (n, hq, dh) or block_tables.shape[0] != n or seq_lens.shape[0] != n:
         raise ValueError("attention tensors: shapes disagree")
+    if not workspace.is_contiguous() or workspace.device != pool.device:
+        raise ValueError("attention workspace: not a contiguous tensor on the pool's device")
     _check(_lib.flowkv_decode_attention(
         ctypes.byref(pool.desc), layer, ctypes.c_void_p(q.data_ptr()), n, hq, pool.kv_heads, dh,
         ctypes.c_void_p(block_tables.data_ptr()), block_tables.shape[1],
