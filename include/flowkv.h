@@ -16,6 +16,11 @@
  *                     K and V, in the per-layer layout (L, 2, B, H) or the
  *                     block-major layout (B, L, 2, H) of Eq. 5, on one GPU.
  *
+ * Beside them: flowkv_decode_attention*, the paged decode attention that
+ * reads either layout (the PagedAttention kernel section 3.3 adapts), and
+ * flowkv_sched*, the load-aware scheduler of section 3.4 (Algorithm 1),
+ * host only.
+ *
  * Conventions for every entry point:
  *   - Functions return FLOWKV_OK (0) or a negative FLOWKV_E* code; nothing
  *     throws across the ABI.  flowkv_strerror() names a code;
@@ -23,10 +28,11 @@
  *   - On error, output arguments are left untouched, except *n_out of the
  *     planners on FLOWKV_ECAP.
  *   - The caller owns every buffer.  The library allocates no device memory and
- *     keeps no pointer after a call returns, except inside an allocator handle.
+ *     keeps no pointer after a call returns, except inside an allocator or a
+ *     scheduler handle.
  *   - Block IDs and counts are int32; byte sizes and offsets are 64-bit.
- *   - Allocator handles are not thread-safe; planners and the transfer are
- *     reentrant.
+ *   - Allocator and scheduler handles are not thread-safe; planners, the
+ *     transfer and attention are reentrant.
  */
 #ifndef FLOWKV_H
 #define FLOWKV_H

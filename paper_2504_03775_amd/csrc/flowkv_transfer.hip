@@ -10,8 +10,10 @@
 // Work decomposition.  A plan covers total_blocks logical blocks; block g's
 // bytes are split into tiles_per_block tiles, giving
 // units = total_blocks * tiles_per_block tiles, walked grid-stride (by
-// default one tile per workgroup), so the workgroups resident at one moment
-// stream one window of neighbouring tiles.  A workgroup finds the run holding
+// default one tile per workgroup).  By default the blocks are visited in a
+// fixed scattered order (x -> x * m mod total_blocks), so the workgroups
+// resident at one moment spread over the whole plan instead of streaming
+// one window of neighbouring tiles.  A workgroup finds the run holding
 // its tile by a galloping search over the runs' `first` fields, starting
 // where equal-length runs would put it: O(log distance) per jump, nothing
 // while it stays inside a run.
