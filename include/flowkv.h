@@ -255,7 +255,7 @@ int flowkv_transfer_layers(const flowkv_pool* src, const flowkv_pool* dst,
 
 #define FLOWKV_ATTN_MAX_SPLIT 1024     /* most tokens per pass-1 workgroup    */
 #define FLOWKV_ATTN_MIN_AUTO_SPLIT 256 /* least tokens the default rule picks */
-#define FLOWKV_ATTN_AUTO_PAIRS 1024    /* (request, split) pairs it aims at   */
+#define FLOWKV_ATTN_AUTO_PAIRS 512     /* (request, split) pairs it aims at   */
 
 /* The split length used when split_tokens is 0: the smallest power of two s
    from FLOWKV_ATTN_MIN_AUTO_SPLIT to FLOWKV_ATTN_MAX_SPLIT with

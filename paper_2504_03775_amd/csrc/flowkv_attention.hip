@@ -411,6 +411,280 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
   }
 }
 
+// Pass 1 on the matrix cores, head_dim 128 (FlowKV section 3.3's consumer,
+// the same arithmetic as decode_attn_split up to rounding order).  Each wave
+// takes its own tiles of 32 tokens; per tile:
+//   - q.k: S (16 x 32, rows = query heads, padded past G) = Q (16 x 128) K^T
+//     as 2 x 4 bf16 MFMAs (16x16x32).  A lane's K load is directly the B
+//     operand: 16 bytes of one token (lane % 16) at dims 32 i + 8 (lane / 16).
+//   - online softmax in the MFMA output layout: a lane holds 4 heads (rows
+//     4 (lane / 16) + j) of 2 tokens; row maxima by DPP rotations over the
+//     16-lane row; the same lazy reference max as the vector kernel.
+//   - P goes through a small LDS transpose into the A operand and is split
+//     into two bf16 parts (hi = bf16(P), lo = bf16(P - hi)), so P.V keeps
+//     about 16 significant bits: O += P_hi V + P_lo V, 2 x 8 MFMAs.
+//   - V lands in LDS straight from memory (global_load_lds, 16 bytes per
+//     lane, no registers) and is read transposed as the B operand; the
+//     contraction runs over tokens in the permuted order k = 8 q + e <->
+//     token 4 e + q on both operands.  The compiler does not track these
+//     loads for LDS reads, so the wave waits for them explicitly.
+// The waves' partial (max, sum, weighted V) merge through LDS at the end.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int kCtrl>
+__device__ __forceinline__ float dpp_max(float x) { return fmaxf(x, dpp<kCtrl>(x)); }
+
+template <int kG, bool kLM>
+__global__ __launch_bounds__(kThreads) void decode_attn_split_mfma(const AttnArgs a) {
+  constexpr int kDh = 128;
+  constexpr int kWaves = kThreads / 64;
+  constexpr int kTile = 32;                      // tokens per wave step
+  constexpr int kVBytes = 8 * 1024;              // LDS bytes of a wave's V tile
+  constexpr int kStep = kWaves * kTile;          // tokens per workgroup step
+  static_assert(kG == 4 || kG == 8, "matrix-core pass for 4 or 8 heads per KV head");
+  const int g = blockIdx.x, split = blockIdx.y, r = blockIdx.z;
+  const int tid = threadIdx.x, wave = tid >> 6, ln = tid & 63;
+  const int q4 = ln >> 4, c16 = ln & 15;         // MFMA lane coordinates
+
+  const int t0 = split * a.split_tokens;
+  const int bs = a.block_size;
+  __shared__ int32_t s_blk[FLOWKV_ATTN_MAX_SPLIT + 1];
+  const int b0 = t0 / bs;
+  {
+    const int span = (t0 + a.split_tokens - 1) / bs - b0 + 1;
+    const int nb = span < a.max_blocks - b0 ? span : a.max_blocks - b0;
+    for (int i = tid; i < nb; i += kThreads)
+      s_blk[i] = a.tables[int64_t(r) * a.max_blocks + b0 + i];
+  }
+  const int T = clamp_len(a, a.seq_lens[r]);
+  if (t0 >= T) return;  // uniform: this split is past the request's end
+  const int t1 = t0 + a.split_tokens < T ? t0 + a.split_tokens : T;
+
+  // Q as the A operand of q.k: Q[head c16][32 i + 8 q4 .. + 8]; rows past G are zero
+  bf16x8 qa[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    u32x4 w = u32x4{0, 0, 0, 0};
+    if (c16 < kG)
+      w = *reinterpret_cast<const u32x4*>(a.q + (int64_t(r) * a.q_heads + g * kG + c16) * kDh +
+                                          32 * i + 8 * q4);
+    qa[i] = __builtin_bit_cast(bf16x8, w);
+  }
+
+  const char* kbase;
+  uint32_t bstride;
+  int64_t voff;
+  if constexpr (kLM) {
+    kbase = a.base[a.layer];
+    bstride = uint32_t(a.chunk_bytes);
+    voff = a.pool_blocks * a.chunk_bytes;
+  } else {
+    kbase = a.base[0] + int64_t(a.layer) * 2 * a.chunk_bytes;
+    bstride = uint32_t(a.block_bytes);
+    voff = a.chunk_bytes;
+  }
+  const uint32_t sstride = uint32_t(a.kv_heads) * kDh * 2;
+  kbase += g * kDh * 2 + 16 * q4;
+
+  // each lane follows two tokens of its wave's tile: 16 gg + c16
+  int tok[2], bi[2], sl[2];
+#pragma unroll
+  for (int gg = 0; gg < 2; ++gg) {
+    tok[gg] = t0 + wave * kTile + 16 * gg + c16;
+    bi[gg] = tok[gg] / bs - b0;
+    sl[gg] = tok[gg] % bs;
+  }
+  const int step_q = kStep / bs, step_r = kStep % bs;
+
+  // LDS: per wave a V tile (8 blocks of 1 KB, one per load instruction:
+  // block (gg, i) holds, at lane * 16, the 16 bytes that lane loaded) and the
+  // P transpose; after the loop the V area holds the waves' weighted sums
+  __shared__ __attribute__((aligned(16))) uint8_t s_v[kWaves * kVBytes];
+  __shared__ __attribute__((aligned(16))) float s_pt[kWaves][16][kTile];
+  static_assert(sizeof(float) * kWaves * kG * kDh <= sizeof(s_v), "merge area fits");
+  uint8_t* const my_v = s_v + wave * kVBytes;
+  float(*const my_p)[kTile] = s_pt[wave];
+
+  f32x4 o[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float mref[4], lsum[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    mref[j] = -INFINITY;
+    lsum[j] = 0.f;
+  }
+  __syncthreads();
+
+  for (int base = t0 + wave * kTile; base < t1; base += kStep) {
+    // K and V of the lane's two tokens (branch-free: a token past the end or
+    // outside the pool reads the pool's first slot and is masked below)
+    u32x4 kp[2][4];
+    bool live[2];
+#pragma unroll
+    for (int gg = 0; gg < 2; ++gg) {
+      const bool in = tok[gg] < t1;
+      const int b = s_blk[in ? bi[gg] : 0];
+      live[gg] = in && b >= 0 && b < a.pool_blocks;
+      const char* kp0 = kbase + (live[gg] ? uint64_t(uint32_t(b)) * bstride +
+                                                uint32_t(sl[gg]) * sstride
+                                          : uint64_t(0));
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        kp[gg][i] = Words<4>::load_nt(kp0 + 64 * i);
+        __builtin_amdgcn_global_load_lds(
+            (const __attribute__((address_space(1))) void*)(kp0 + voff + 64 * i),
+            (__attribute__((address_space(3))) void*)(my_v + (gg * 4 + i) * 1024), 16, 0, 0);
+      }
+      tok[gg] += kStep;
+      bi[gg] += step_q;
+      sl[gg] += step_r;
+      if (sl[gg] >= bs) {
+        sl[gg] -= bs;
+        bi[gg] += 1;
+      }
+    }
+
+    // q.k: s[gg][j] = S[head 4 q4 + j][token 16 gg + c16]
+    f32x4 s[2];
+#pragma unroll
+    for (int gg = 0; gg < 2; ++gg) {
+      s[gg] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        s[gg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[i], __builtin_bit_cast(bf16x8, kp[gg][i]),
+                                                        s[gg], 0, 0, 0);
+    }
+    // online softmax per head row
+    bool rescale = false;
+    float c[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float x0 = live[0] ? s[0][j] * a.scale_log2 : -INFINITY;
+      const float x1 = live[1] ? s[1][j] * a.scale_log2 : -INFINITY;
+      s[0][j] = x0;
+      s[1][j] = x1;
+      float cm = fmaxf(x0, x1);
+      cm = dpp_max<kRor8>(cm);
+      cm = dpp_max<kRor4>(cm);
+      cm = dpp_max<0x122>(cm);   // rotate by 2
+      cm = dpp_max<0x121>(cm);   // rotate by 1
+      c[j] = 1.f;
+      if (cm > mref[j] + kLazy) {
+        c[j] = __builtin_amdgcn_exp2f(mref[j] - cm);
+        mref[j] = cm;
+        rescale = true;
+      }
+    }
+    if (rescale) {
+#pragma unroll
+      for (int t = 0; t < 8; ++t)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[t][j] *= c[j];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float mu = mref[j] == -INFINITY ? 0.f : mref[j];
+      const bool real = 4 * q4 + j < kG;
+#pragma unroll
+      for (int gg = 0; gg < 2; ++gg) {
+        const float p = real ? __builtin_amdgcn_exp2f(s[gg][j] - mu) : 0.f;
+        lsum[j] = fmaf(lsum[j], gg == 0 ? c[j] : 1.f, p);
+        // P[head][token] at the A operand's position of token 16 gg + c16
+        my_p[4 * q4 + j][8 * (c16 & 3) + 4 * gg + (c16 >> 2)] = p;
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+
+    // the V tile is in LDS once this wave's loads have all returned; masked
+    // tokens' rows are then zeroed (their weight is 0, and 0 x a stale NaN
+    // would not be)
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (!live[0] || !live[1]) {
+#pragma unroll
+      for (int gg = 0; gg < 2; ++gg)
+        if (!live[gg])
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            *reinterpret_cast<u32x4*>(my_v + (gg * 4 + i) * 1024 + ln * 16) = u32x4{0, 0, 0, 0};
+    }
+    asm volatile("" ::: "memory");
+    // A operand: P[head c16][k = 8 q4 + e], token 4 e + q4, split in two bf16
+    bf16x8 ahi, alo;
+    {
+      const float4 p0 = *reinterpret_cast<const float4*>(&my_p[c16][8 * q4]);
+      const float4 p1 = *reinterpret_cast<const float4*>(&my_p[c16][8 * q4 + 4]);
+      const float pa[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const __bf16 h = (__bf16)pa[e];
+        ahi[e] = h;
+        alo[e] = (__bf16)(pa[e] - (float)h);
+      }
+    }
+    // B operand per 16-dim tile: V[token 4 e + q4][dim 16 t + c16]
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      bf16x8 bv;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int tk = 4 * e + q4, bo = (16 * t + c16) * 2;
+        bv[e] = *reinterpret_cast<const __bf16*>(
+            my_v + ((tk >> 4) * 4 + (bo >> 6)) * 1024 + (16 * ((bo >> 4) & 3) + (tk & 15)) * 16 +
+            (bo & 15));
+      }
+      o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bv, o[t], 0, 0, 0);
+      o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bv, o[t], 0, 0, 0);
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+
+  // merge the 4 waves: per head a weight exp2(m_wave - M)
+  __shared__ float s_m[kWaves][16], s_l[kWaves][16], s_w[kWaves][16];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float l = lsum[j];
+    l += dpp<kRor8>(l);
+    l += dpp<kRor4>(l);
+    l += dpp<0x122>(l);
+    l += dpp<0x121>(l);
+    if (c16 == 0) {
+      s_m[wave][4 * q4 + j] = mref[j];
+      s_l[wave][4 * q4 + j] = l;
+    }
+  }
+  __syncthreads();  // every wave is past the loop: the V area is free
+  float* const s_o = reinterpret_cast<float*>(s_v);   // [wave][head < kG][dim]
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (4 * q4 + j < kG) s_o[(wave * kG + 4 * q4 + j) * kDh + 16 * t + c16] = o[t][j];
+  float* const dst0 = a.ws + ((int64_t(r) * a.q_heads + g * kG) * a.max_splits + split) * (kDh + 2);
+  const int64_t head_stride = int64_t(a.max_splits) * (kDh + 2);
+  if (tid < kG) {
+    float M = -INFINITY;
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][tid]);
+    float L = 0.f;
+    for (int w = 0; w < kWaves; ++w) {
+      const float wt = s_m[w][tid] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s_m[w][tid] - M);
+      s_w[w][tid] = wt;
+      L = fmaf(s_l[w][tid], wt, L);
+    }
+    dst0[tid * head_stride] = M;
+    dst0[tid * head_stride + 1] = L;
+  }
+  __syncthreads();
+  for (int i = tid; i < kG * kDh; i += kThreads) {
+    const int h = i / kDh, d = i % kDh;
+    float A = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) A = fmaf(s_o[(w * kG + h) * kDh + d], s_w[w][h], A);
+    dst0[h * head_stride + 2 + d] = A;
+  }
+}
+
 // Pass 2: one workgroup per (query head, request).  The largest split
 // reference comes first (all threads over the splits, then across the
 // workgroup); then 256 / Dh thread sets each take every (256 / Dh)-th split,
@@ -479,6 +753,10 @@ SplitFn pick_group(int G) {
 }
 
 SplitFn pick_split(int D, int G, bool lm) {
+  // 8 query heads per KV head at head_dim 128: the matrix-core pass (the
+  // vector pass is near its ALU limit there)
+  if (D == 128 && G == 8)
+    return lm ? decode_attn_split_mfma<8, true> : decode_attn_split_mfma<8, false>;
   if (D == 64) return lm ? pick_group<64, true>(G) : pick_group<64, false>(G);
   return lm ? pick_group<128, true>(G) : pick_group<128, false>(G);
 }

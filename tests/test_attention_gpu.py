@@ -4,8 +4,11 @@ Tolerance, from the arithmetic: K, V and q are bfloat16 (exact in float32);
 scores are float32 dot products of head_dim terms (relative error a few
 1e-6), softmax weights use float32 exp2 (about 1 ulp), and the weighted sums
 of V accumulate at most ~1,300 float32 terms per lane group before the
-merges (relative error below 1e-4 of the weighted |V| mean).  So every output
-element must satisfy |out - oracle| <= 2e-4 * max|V| + 1e-6.
+merges (relative error below 1e-4 of the weighted |V| mean).  The
+matrix-core pass (8 query heads per KV head, head_dim 128) carries each
+weight into P.V as two bfloat16 parts, hi + lo, which keep it to a relative
+2^-16 (1.5e-5).  So every output element must satisfy
+|out - oracle| <= 2e-4 * max|V| + 1e-6.
 """
 
 import sys

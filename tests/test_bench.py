@@ -87,5 +87,5 @@ def test_attention_line_contract():
                 "roofline"):
         assert key in j, key
     assert j["config"]["kv_heads"] == 1 and j["config"]["q_heads"] == 8
-    assert j["config"]["split_tokens"] == 512 and j["value"] > 0
+    assert j["config"]["split_tokens"] == 1024 and j["value"] > 0
     assert j["roofline"]["bound"] == "hbm"

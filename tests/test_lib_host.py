@@ -48,13 +48,13 @@ def test_binding_constants_match_the_header():
 
 def test_attention_split_rule_and_workspace():
     """The default split: the smallest power of two from 256 to 1024 giving at
-    most 1024 (request, split) pairs; the workspace follows it."""
-    cases = {(1, 13000): 256, (1, 400000): 512, (32, 20000): 1024, (16, 32000): 512,
-             (32, 8192): 256, (33, 8192): 512, (0, 5): 256, (3, 0): 256, (2000, 100): 1024}
+    most 512 (request, split) pairs; the workspace follows it."""
+    cases = {(1, 13000): 256, (1, 200000): 512, (32, 20000): 1024, (16, 32000): 1024,
+             (16, 8192): 256, (17, 8192): 512, (0, 5): 256, (3, 0): 256, (2000, 100): 1024}
     for (n, T), want in cases.items():
         got = fk.flowkv_decode_attention_split(n, T)
         assert got == want, (n, T, got)
-        brute = next((s for s in (256, 512) if n * -(-T // s) <= 1024), 1024)
+        brute = next((s for s in (256, 512) if n * -(-T // s) <= 512), 1024)
         assert got == brute
         ws = fk.flowkv_decode_attention_workspace(n, 32, 128, T)
         assert ws == n * 32 * -(-T // got) * 130 * 4
