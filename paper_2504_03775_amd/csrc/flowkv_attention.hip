@@ -532,7 +532,10 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split_mfma(const AttnArg
                                           : uint64_t(0));
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        kp[gg][i] = Words<4>::load_nt(kp0 + 64 * i);
+        // cached, not nontemporal: each load reads half of a 128-byte line
+        // and the next one the other half; with nontemporal loads the line
+        // was often gone in between (9% more HBM traffic, measured)
+        kp[gg][i] = *(const gvec4*)(kp0 + 64 * i);
         __builtin_amdgcn_global_load_lds(
             (const __attribute__((address_space(1))) void*)(kp0 + voff + 64 * i),
             (__attribute__((address_space(3))) void*)(my_v + (gg * 4 + i) * 1024), 16, 0, 0);
