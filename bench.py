@@ -373,8 +373,8 @@ def bench_schedule(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the transfer "
-              "path in this build is single-device.", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): both pools of "
+              "the transfer live on one device.", file=sys.stderr)
         sys.exit(2)
     if args.op == "attention":
         bench_attention(args)

@@ -8,8 +8,8 @@ blocks, which the receiver names with its own block-ID list (Figure 3
 caption).  Eq. 5 gives the two pool layouts:
 
 * layer-major ``(L, 2, B, H)`` -- one tensor per layer holding K (index 0) and
-  V (index 1) for all ``B`` blocks; this build stores each layer as its own
-  buffer, as per-layer paged tensors are allocated;
+  V (index 1) for all ``B`` blocks; each layer is its own buffer here, as
+  per-layer paged tensors are allocated;
 * block-major ``(B, L, 2, H)`` -- every layer's K and V of one block adjacent.
 
 ``H`` (the "remaining KV vector" of one block) is read as
