@@ -1,5 +1,5 @@
 """Shared plumbing for the GPU parity tests: pools on the device, downloads
-into the oracle's host pools, and the sampled comparison used at full size.
+into the oracle's host pools, and the comparison used at full size.
 
 Expected values always come from ``oracle`` run on host copies of device
 memory that the transfer kernel has not touched yet (the seeded source pool
@@ -96,12 +96,38 @@ def check_full_pool(geom, sl, dl, src_blocks, dst_blocks, tables, seed=0, **cfg)
     return segs
 
 
+def gather_blocks(pool: fk.KVPool, idx: torch.Tensor) -> torch.Tensor:
+    """Blocks `idx` of a device pool as bytes, (len(idx), L, 2, chunk), in
+    either layout; torch's own indexing, nothing from the library."""
+    n, L = idx.numel(), pool.num_layers
+    if pool.layout == BM:
+        return pool.tensors[0].index_select(0, idx).view(torch.uint8).reshape(n, L, 2, -1)
+    per_layer = [t.index_select(1, idx).view(torch.uint8).reshape(2, n, -1) for t in pool.tensors]
+    return torch.stack(per_layer, 0).permute(2, 0, 1, 3)
+
+
+def moved_blocks_equal(src: fk.KVPool, dst: fk.KVPool, S, D) -> bool:
+    """Every moved block, whole, on the device: receiver block D[i] equals
+    sender block S[i] in every layer and both of K and V.  With whole-block
+    semantics this is the copy's definition at block granularity, so it holds
+    at any size; pieces of about 256 MiB per side keep it within free memory."""
+    S_t = torch.as_tensor(np.asarray(S, dtype=np.int64), device=src.device)
+    D_t = torch.as_tensor(np.asarray(D, dtype=np.int64), device=dst.device)
+    step = max(1, (256 << 20) // src.block_bytes)
+    for lo in range(0, S_t.numel(), step):
+        if not torch.equal(gather_blocks(src, S_t[lo:lo + step]),
+                           gather_blocks(dst, D_t[lo:lo + step])):
+            return False
+    return True
+
+
 def check_sampled(wl, wl_ref, sl, dl, max_blocks=1536, untouched_frac=0.01, max_untouched=1024,
                   seed_sample=7, **cfg):
-    """Full-size comparison on samples: a seeded sample of the moved blocks
-    (all of them when there are at most max_blocks) against the oracle, and
-    the guard blocks around every receiver run plus a seeded sample of the
-    other receiver blocks against their pre-image.
+    """Full-size comparison: a seeded sample of the moved blocks (all of them
+    when there are at most max_blocks) against the oracle; every moved block
+    against its sender block on the device (`moved_blocks_equal`); and the
+    guard blocks around every receiver run plus a seeded sample of the other
+    receiver blocks against their pre-image.
 
     `wl` holds the block lists from the library's allocator (they drive the
     device path), `wl_ref` the same workload from the oracle's allocator
@@ -144,6 +170,7 @@ def check_sampled(wl, wl_ref, sl, dl, max_blocks=1536, untouched_frac=0.01, max_
     assert host_equal(got, expect), first_mismatch(got, expect)
     after = download_blocks(dst, keep)
     assert host_equal(after, before), first_mismatch(after, before)
+    assert moved_blocks_equal(src, dst, S, D)
     del src, dst
     torch.cuda.empty_cache()
     return segs, len(pick), len(keep)

@@ -1,8 +1,9 @@
 """GPU parity: the one-launch transfer kernel against the oracle, byte-exact.
 
-Small pools are compared whole; the full-size workloads on seeded samples of
-the moved blocks, every guard block around a receiver run and a seeded 1%
-sample of the untouched receiver blocks.  Every case goes through the C ABI
+Small pools are compared whole.  At full size, a seeded sample of the moved
+blocks is compared with the oracle, every moved block with its sender block
+on the device, and every guard block around a receiver run plus a seeded 1%
+sample of the untouched receiver blocks with their pre-image.  Every case goes through the C ABI
 (allocator, planner, transfer) via the ctypes binding.
 """
 
