@@ -283,7 +283,7 @@ int flowkv_decode_attention_workspace(int32_t n_req, int32_t q_heads, int32_t he
    aligned; block_tables (n_req, max_blocks) int32; seq_lens (n_req) int32.
    Output: out (n_req, q_heads, head_dim) float32.  workspace: device memory
    of at least flowkv_decode_attention_workspace(...) bytes, owned by the
-   caller, busy until the stream passes the call.  Tokens beyond
+   caller, busy until the stream passes the call (NULL when that is 0).  Tokens beyond
    max_blocks x block_size or beyond max_seq_len are not read; a block ID
    outside the pool contributes nothing; a request with no tokens gets zeros.
    head_dim 64 or 128; q_heads / kv_heads in {1, 2, 4, 8}; split_tokens 0 =

@@ -842,9 +842,10 @@ extern "C" int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer,
                 FLOWKV_ATTN_MAX_SPLIT);
   if (!(scale > 0.f) || !std::isfinite(scale)) return fail(FLOWKV_EINVAL, "bad scale");
   if (n_req == 0) return ok();
-  if (!q_dev || !block_tables_dev || !seq_lens_dev || !out_dev || !workspace_dev)
-    return fail(FLOWKV_EINVAL, "NULL device pointer");
   const int64_t need = ws_bytes(n_req, q_heads, head_dim, max_seq_len, split_tokens);
+  // (a workspace of 0 bytes, when max_seq_len is 0, may be NULL)
+  if (!q_dev || !block_tables_dev || !seq_lens_dev || !out_dev || (!workspace_dev && need > 0))
+    return fail(FLOWKV_EINVAL, "NULL device pointer");
   if (workspace_bytes < need)
     return fail(FLOWKV_ECAP, "workspace of %lld bytes, %lld needed", (long long)workspace_bytes,
                 (long long)need);

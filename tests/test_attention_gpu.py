@@ -159,6 +159,10 @@ def test_length_caps_and_empty_request():
     assert err is not None
     z, _ = run_case(geom, LM, 40, [0, 50], 4, 4, check=False)
     assert np.all(z[0] == 0)
+    # max_seq_len 0: no token is read, every output is zero, and the
+    # workspace has 0 bytes (a NULL pointer is accepted)
+    z, _ = run_case(geom, BM, 40, [30, 50], 4, 5, max_seq=0, check=False)
+    assert np.all(z == 0)
 
 
 @pytest.mark.parametrize("layout", [BM, LM], ids=lambda x: NAMES[x])
