@@ -89,3 +89,20 @@ def test_attention_line_contract():
     assert j["config"]["kv_heads"] == 1 and j["config"]["q_heads"] == 8
     assert j["config"]["split_tokens"] == 1024 and j["value"] > 0
     assert j["roofline"]["bound"] == "hbm"
+
+
+@pytest.mark.gpu
+def test_overlap_line_contract():
+    """bench.py --op overlap: the prefill stand-in alone and with the three
+    transfer forms, each timed; one JSON line in the same contract."""
+    j = run_bench("--op", "overlap", "--steps", "2", "--warmup", "1")
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
+                "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config",
+                "roofline", "cpu_baseline"):
+        assert key in j, key
+    assert j["unit"] == "ms" and j["higher_is_better"] is False
+    assert set(j["median_ms"]) == {"prefill", "one_launch_after", "layerwise_overlap",
+                                   "layerwise_after"}
+    assert all(v > 0 for v in j["median_ms"].values())
+    assert j["value"] == j["exposed_ms"]["layerwise_overlap"]
+    assert j["config"]["tokens"] == 13000 and j["config"]["layers"] == 32
