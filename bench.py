@@ -143,6 +143,20 @@ ATTN_WORKLOADS = {
 }
 
 
+RESERVE_BYTES = 4 << 30   # device memory left free beside the pools
+
+
+def fit_receiver_blocks(free_bytes: int, src_blocks: int, dst_blocks: int,
+                        block_bytes: int, reserve: int = RESERVE_BYTES) -> int:
+    """Receiver-pool size that fits beside the sender's pool: dst_blocks if
+    both fit in free_bytes - reserve, else the largest multiple of 4,096
+    blocks that does (0 if not even 4,096 fit)."""
+    room = free_bytes - reserve - src_blocks * block_bytes
+    if room >= dst_blocks * block_bytes:
+        return dst_blocks
+    return max(0, room // block_bytes // 4096 * 4096)
+
+
 def bench_attention(args):
     """Decode attention (one layer, one new token per request) over the
     receiver pool and block lists of a transfer workload: by default the
@@ -584,8 +598,19 @@ def main():
     # ---- setup (untimed): block lists, pools ------------------------------------
     make_alloc = lambda P, pol, seed: fk.Allocator(P, pol, seed)  # noqa: E731
     recipe, rargs, wl_desc = WORKLOADS[args.workload]
+    shrunk = None
     if single:
         wl = recipes.llama8b_13k(make_alloc, args.dst_policy)
+        # a device without room for both 65,536-block pools gets a smaller
+        # receiver pool (the request's 813 blocks still fit at 30% occupancy)
+        free, _ = torch.cuda.mem_get_info()
+        fit = fit_receiver_blocks(free, wl.src_pool_blocks, wl.dst_pool_blocks,
+                                  wl.geom.block_bytes)
+        if 0 < fit < wl.dst_pool_blocks:
+            shrunk = {"receiver_pool_blocks_from": wl.dst_pool_blocks, "to": fit,
+                      "reason": f"{free / 2**30:.1f} GiB of device memory free"}
+            print(f"receiver pool shrunk to {fit} blocks: {shrunk['reason']}", file=sys.stderr)
+            wl = recipes.llama8b_13k(make_alloc, args.dst_policy, dst_pool_blocks=fit)
     elif recipe == "tiny":
         wl = recipes.tiny()
     else:
@@ -599,7 +624,7 @@ def main():
 
     free, _ = torch.cuda.mem_get_info()
     need = (src_blocks + dst_blocks) * geom.block_bytes
-    if need > free - (4 << 30):
+    if need > free - RESERVE_BYTES:
         raise SystemExit(f"pools need {need / 2**30:.1f} GiB, {free / 2**30:.1f} GiB free")
     t0 = time.perf_counter()
     src = fk.KVPool(layout, make_device_pool(geom, layout, src_blocks, dev, seed=0))
@@ -848,6 +873,8 @@ def main():
               "runs": n_runs}
     if single:
         config.update(receiver_policy=args.dst_policy, receiver_occupied=0.30)
+        if shrunk:
+            config["receiver_pool_shrunk"] = shrunk
     if args.layerwise:
         config.update(launches_per_step=geom.num_layers, mode="layer-wise")
     config["plan_in"] = ("kernel-arguments" if n_runs <= fk.INLINE_RUNS and not args.layerwise

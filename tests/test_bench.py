@@ -56,6 +56,28 @@ def test_bench_line_contract_on_tiny(layout):
     assert cb["kind"] == "oracle" and cb["cores"] >= 1 and cb["value"] > 0
 
 
+def test_receiver_pool_shrinks_to_fit():
+    """Where the device cannot hold both 65,536-block pools of the 13k
+    request, the receiver's pool shrinks to the largest multiple of 4,096
+    blocks that fits beside the sender's (and the request still fits)."""
+    import bench
+    from paper_2504_03775_amd import flowkv as fk
+    from workloads import recipes
+
+    BB, GiB = 2 << 20, 1 << 30
+    r = bench.RESERVE_BYTES
+    assert bench.fit_receiver_blocks(300 * GiB, 65536, 65536, BB) == 65536
+    assert bench.fit_receiver_blocks(256 * GiB + r, 65536, 65536, BB) == 65536
+    assert bench.fit_receiver_blocks(256 * GiB + r - 1, 65536, 65536, BB) == 61440
+    assert bench.fit_receiver_blocks(200 * GiB + r, 65536, 65536, BB) == 36864
+    assert bench.fit_receiver_blocks(128 * GiB + r + 4095 * BB, 65536, 65536, BB) == 0
+    wl = recipes.llama8b_13k(lambda P, pol, seed: fk.Allocator(P, pol, seed), "segment",
+                             dst_pool_blocks=36864)
+    (S, D), = wl.tables
+    assert wl.src_pool_blocks == 65536 and wl.dst_pool_blocks == 36864
+    assert len(D) == 813 and D.max() < 36864 and len(set(D.tolist())) == 813
+
+
 def test_schedule_line_contract_on_cpu():
     """bench.py --op schedule runs on the host alone: one JSON line with the
     scheduler's rate, the oracle beside it and the cluster model's mixes."""
