@@ -53,7 +53,9 @@ enum {
   FLOWKV_EDUP = -4,   /* a block ID repeated where it must be unique, freeing
                          a free block, or marking a used block               */
   FLOWKV_ECAP = -5,   /* output capacity too small; *n_out holds the need     */
-  FLOWKV_EHIP = -6    /* the HIP runtime refused the launch                   */
+  FLOWKV_EHIP = -6,   /* the HIP runtime refused the launch                   */
+  FLOWKV_ENOMEM = -7  /* host memory ran out; an allocator or scheduler handle
+                         that returned it may be inconsistent: destroy it     */
 };
 
 /* ---- allocator policies ---------------------------------------------------- */

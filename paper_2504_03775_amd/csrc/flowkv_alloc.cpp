@@ -129,7 +129,7 @@ extern "C" int flowkv_allocator_create(int32_t num_blocks, int32_t policy, uint6
       policy != FLOWKV_POLICY_FIFO_SHUFFLED)
     return fail(FLOWKV_EINVAL, "unknown allocator policy %d", policy);
   auto* a = new (std::nothrow) flowkv_allocator();
-  if (!a) return fail(FLOWKV_EINVAL, "out of host memory");
+  if (!a) return fail(FLOWKV_ENOMEM, "out of host memory");
   try {
     a->num_blocks = num_blocks;
     a->policy = policy;
@@ -151,7 +151,7 @@ extern "C" int flowkv_allocator_create(int32_t num_blocks, int32_t policy, uint6
     }
   } catch (const std::bad_alloc&) {
     delete a;
-    return fail(FLOWKV_EINVAL, "out of host memory");
+    return fail(FLOWKV_ENOMEM, "out of host memory");
   }
   *out = a;
   return ok();
@@ -159,7 +159,9 @@ extern "C" int flowkv_allocator_create(int32_t num_blocks, int32_t policy, uint6
 
 extern "C" void flowkv_allocator_destroy(flowkv_allocator* a) { delete a; }
 
-extern "C" int flowkv_alloc(flowkv_allocator* a, int32_t n, int32_t* out_ids) {
+namespace {
+
+int alloc_impl(flowkv_allocator* a, int32_t n, int32_t* out_ids) {
   if (!a) return fail(FLOWKV_EINVAL, "NULL allocator");
   if (n < 0) return fail(FLOWKV_EINVAL, "negative block count %d", n);
   if (n > 0 && !out_ids) return fail(FLOWKV_EINVAL, "NULL output list");
@@ -198,7 +200,7 @@ extern "C" int flowkv_alloc(flowkv_allocator* a, int32_t n, int32_t* out_ids) {
   return ok();
 }
 
-extern "C" int flowkv_free(flowkv_allocator* a, const int32_t* ids, int32_t n) {
+int free_impl(flowkv_allocator* a, const int32_t* ids, int32_t n) {
   if (!a) return fail(FLOWKV_EINVAL, "NULL allocator");
   std::vector<int32_t> s;
   int rc = check_ids(a, ids, n, /*want_used=*/true, s);
@@ -212,7 +214,7 @@ extern "C" int flowkv_free(flowkv_allocator* a, const int32_t* ids, int32_t n) {
   return ok();
 }
 
-extern "C" int flowkv_mark_used(flowkv_allocator* a, const int32_t* ids, int32_t n) {
+int mark_used_impl(flowkv_allocator* a, const int32_t* ids, int32_t n) {
   if (!a) return fail(FLOWKV_EINVAL, "NULL allocator");
   std::vector<int32_t> s;
   int rc = check_ids(a, ids, n, /*want_used=*/false, s);
@@ -228,6 +230,20 @@ extern "C" int flowkv_mark_used(flowkv_allocator* a, const int32_t* ids, int32_t
     a->fifo.swap(kept);
   }
   return ok();
+}
+
+}  // namespace
+
+extern "C" int flowkv_alloc(flowkv_allocator* a, int32_t n, int32_t* out_ids) {
+  return flowkv::guarded([&] { return alloc_impl(a, n, out_ids); });
+}
+
+extern "C" int flowkv_free(flowkv_allocator* a, const int32_t* ids, int32_t n) {
+  return flowkv::guarded([&] { return free_impl(a, ids, n); });
+}
+
+extern "C" int flowkv_mark_used(flowkv_allocator* a, const int32_t* ids, int32_t n) {
+  return flowkv::guarded([&] { return mark_used_impl(a, ids, n); });
 }
 
 extern "C" int flowkv_allocator_stats(const flowkv_allocator* a, flowkv_alloc_stats* out) {

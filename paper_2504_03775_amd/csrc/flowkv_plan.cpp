@@ -129,14 +129,18 @@ extern "C" int flowkv_plan(const int32_t* src_ids, const int32_t* dst_ids, int32
                            flowkv_segment* out, int64_t cap, int64_t* n_out) {
   if (n_blocks < 0) return fail(FLOWKV_EINVAL, "negative block count %d", n_blocks);
   const int64_t offsets[2] = {0, n_blocks};
-  return plan_impl(1, offsets, src_ids, dst_ids, src_pool_blocks, dst_pool_blocks, out, cap,
-                   n_out);
+  return flowkv::guarded([&] {
+    return plan_impl(1, offsets, src_ids, dst_ids, src_pool_blocks, dst_pool_blocks, out, cap,
+                     n_out);
+  });
 }
 
 extern "C" int flowkv_plan_batch(int32_t n_req, const int64_t* offsets, const int32_t* src_ids,
                                  const int32_t* dst_ids, int32_t src_pool_blocks,
                                  int32_t dst_pool_blocks, flowkv_segment* out, int64_t cap,
                                  int64_t* n_out) {
-  return plan_impl(n_req, offsets, src_ids, dst_ids, src_pool_blocks, dst_pool_blocks, out, cap,
-                   n_out);
+  return flowkv::guarded([&] {
+    return plan_impl(n_req, offsets, src_ids, dst_ids, src_pool_blocks, dst_pool_blocks, out,
+                     cap, n_out);
+  });
 }

@@ -60,7 +60,7 @@ extern "C" int flowkv_sched_create(const flowkv_sched_params* params, int32_t n_
   for (int32_t i = 0; i < n_nodes; ++i)
     if (!valid_role(roles[i])) return fail(FLOWKV_EINVAL, "role of node %d is %d", i, roles[i]);
   flowkv_sched* s = new (std::nothrow) flowkv_sched;
-  if (!s) return fail(FLOWKV_ENOSPC, "out of host memory");
+  if (!s) return fail(FLOWKV_ENOMEM, "out of host memory");
   try {
     s->p = p;
     s->n = n_nodes;
@@ -69,7 +69,7 @@ extern "C" int flowkv_sched_create(const flowkv_sched_params* params, int32_t n_
     s->scores.assign(size_t(n_nodes) * 2, 0.0);
   } catch (const std::bad_alloc&) {
     delete s;
-    return fail(FLOWKV_ENOSPC, "out of host memory");
+    return fail(FLOWKV_ENOMEM, "out of host memory");
   }
   *out = s;
   return ok();

@@ -33,6 +33,7 @@ extern "C" const char* flowkv_strerror(int code) {
     case FLOWKV_EDUP: return "block ID repeated, already free or already in use";
     case FLOWKV_ECAP: return "output capacity too small";
     case FLOWKV_EHIP: return "HIP runtime error";
+    case FLOWKV_ENOMEM: return "out of host memory";
     default: return "unknown status code";
   }
 }

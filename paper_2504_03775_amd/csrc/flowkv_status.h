@@ -4,6 +4,7 @@
 
 #include <cstdarg>
 #include <cstdint>
+#include <new>
 
 #include "flowkv.h"
 
@@ -14,5 +15,19 @@ int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 
 // Clear the calling thread's message and return FLOWKV_OK.
 int ok();
+
+// Run an entry point's body so that no exception crosses the C ABI: the
+// standard containers of the host code can only raise std::bad_alloc, which
+// becomes FLOWKV_ENOMEM.
+template <class F>
+int guarded(F&& body) {
+  try {
+    return body();
+  } catch (const std::bad_alloc&) {
+    return fail(FLOWKV_ENOMEM, "out of host memory");
+  } catch (...) {
+    return fail(FLOWKV_EINVAL, "unexpected host exception");
+  }
+}
 
 }  // namespace flowkv

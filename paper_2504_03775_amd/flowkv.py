@@ -20,7 +20,7 @@ import numpy as np
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libflowkv.so")
 
-OK, EINVAL, ENOSPC, ERANGE, EDUP, ECAP, EHIP = 0, -1, -2, -3, -4, -5, -6
+OK, EINVAL, ENOSPC, ERANGE, EDUP, ECAP, EHIP, ENOMEM = 0, -1, -2, -3, -4, -5, -6, -7
 POLICY_SEGMENT, POLICY_FIFO_SORTED, POLICY_FIFO_SHUFFLED = 0, 1, 2
 LAYOUT_LAYER_MAJOR, LAYOUT_BLOCK_MAJOR = 0, 1
 MAX_LAYERS = 128

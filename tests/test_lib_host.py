@@ -42,7 +42,7 @@ def test_binding_constants_match_the_header():
     defines = dict(re.findall(r"#define\s+(FLOWKV_\w+)\s+(-?\d+)", text))
     assert int(defines["FLOWKV_INLINE_RUNS"]) == fk.INLINE_RUNS
     enums = dict(re.findall(r"\b(FLOWKV_E?\w+)\s*=\s*(-?\d+)", text))
-    for name in ("OK", "EINVAL", "ENOSPC", "ERANGE", "EDUP", "ECAP", "EHIP"):
+    for name in ("OK", "EINVAL", "ENOSPC", "ERANGE", "EDUP", "ECAP", "EHIP", "ENOMEM"):
         assert int(enums["FLOWKV_" + name]) == getattr(fk, name), name
 
 
@@ -67,7 +67,7 @@ def test_attention_split_rule_and_workspace():
 
 
 def test_strerror_names_every_code():
-    for c in (fk.OK, fk.EINVAL, fk.ENOSPC, fk.ERANGE, fk.EDUP, fk.ECAP, fk.EHIP):
+    for c in (fk.OK, fk.EINVAL, fk.ENOSPC, fk.ERANGE, fk.EDUP, fk.ECAP, fk.EHIP, fk.ENOMEM):
         assert fk.strerror(c) and fk.strerror(c) != "unknown status code"
     assert fk.strerror(12345) == "unknown status code"
 
