@@ -206,6 +206,48 @@ def test_plan_contiguous_is_one_and_stride2_is_n():
     assert len(segs) == n
 
 
+def test_planners_are_reentrant_across_threads():
+    """flowkv_plan keeps its duplicate-check bitmaps per thread: many threads
+    planning at once (ctypes releases the interpreter lock during the call)
+    each get the oracle's plan, including right after a rejected plan left
+    bits to clear."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    g = np.random.default_rng(11)
+    cases = []
+    for i in range(16):   # long lists, so calls on different threads overlap in time
+        P = int(g.integers(100_000, 1_000_000))
+        n = int(g.integers(50_000, 200_000))
+        S = np.sort(g.permutation(P)[:n]) if i % 3 else g.permutation(P)[:n]
+        D = np.sort(g.permutation(P)[:n]) if i % 2 else g.permutation(P)[:n]
+        want = np.array(oracle.plan_ref(S.tolist(), D.tolist()), dtype=np.int64).reshape(-1, 3)
+        cases.append((S.astype(np.int32), D.astype(np.int32), P, want))
+
+    def same(segs, want):
+        got = np.stack([segs["src_block"], segs["dst_block"], segs["n_blocks"]], axis=1)
+        return np.array_equal(got, want)
+
+    def worker(t):
+        for k in range(len(cases)):
+            S, D, P, want = cases[(k * 7 + t) % len(cases)]
+            if (k + t) % 5 == 0 and len(D) > 1:   # a repeat: EDUP, bits cleared again
+                bad = D.copy()
+                bad[-1] = bad[0]
+                try:
+                    fk.flowkv_plan(S, bad, P, P)
+                    return f"thread {t}: repeated receiver block accepted"
+                except fk.FlowKVError as e:
+                    if e.code != fk.EDUP:
+                        return f"thread {t}: code {e.code}"
+            if not same(fk.flowkv_plan(S, D, P, P), want):
+                return f"thread {t}: case {(k * 7 + t) % len(cases)} differs"
+        return None
+
+    with ThreadPoolExecutor(8) as ex:
+        errors = [e for e in ex.map(worker, range(8)) if e]
+    assert not errors, errors
+
+
 def test_plan_errors():
     P = 16
     cases = [((P,), (0,), fk.ERANGE), ((0,), (-1,), fk.ERANGE), ((1, 1), (2, 3), fk.EDUP),
