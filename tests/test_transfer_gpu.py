@@ -18,7 +18,8 @@ import oracle
 from paper_2504_03775_amd import flowkv as fk
 from workloads import TINY, LLAMA3_8B, Geometry, random_table, recipes
 from tests.gpu_helpers import (BM, LM, check_full_pool, check_sampled, device_pool,
-                               download_all, host_equal, plan_tables, run_transfer)
+                               download_all, first_mismatch, host_equal, plan_tables,
+                               run_transfer)
 
 pytestmark = pytest.mark.gpu
 
@@ -160,6 +161,56 @@ def test_two_streams_two_plans():
     torch.cuda.synchronize()
     oracle.transfer_fast(h_src, h_dst, [0, 1, 2, 5, 9], [10, 11, 3, 0, 1])
     assert host_equal(download_all(dst), h_dst)
+
+
+def test_launches_from_four_host_threads():
+    """The launcher is reentrant: four host threads each plan and enqueue
+    transfers on a stream of their own at the same time (ctypes releases the
+    interpreter lock during the calls), into disjoint receiver blocks, with
+    both kernel-argument and device plans; the result equals the oracle's."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    geom = Geometry("threads", 4, 2, 64, 16, "float16")     # 32 KiB blocks
+    B = 4096
+    src = device_pool(geom, BM, B, 0)
+    dst = device_pool(geom, LM, B, 1)
+    h_src, h_dst = download_all(src), download_all(dst)
+    g = np.random.default_rng(3)
+    perm_d = g.permutation(B).astype(np.int32)
+    jobs = []   # per thread: 24 requests of 1..40 blocks, receiver blocks disjoint
+    pos = 0
+    for t in range(4):
+        reqs = []
+        for _ in range(24):
+            n = int(g.integers(1, 41))
+            S = (np.arange(n) + int(g.integers(0, B - n))).astype(np.int32) if g.random() < 0.5 \
+                else g.permutation(B)[:n].astype(np.int32)
+            reqs.append((S, perm_d[pos:pos + n]))
+            pos += n
+        jobs.append(reqs)
+
+    def worker(t):
+        stream = torch.cuda.Stream(src.device)
+        keep = []
+        for i, (S, D) in enumerate(jobs[t]):
+            segs = fk.flowkv_plan(S, D, B, B)
+            if i % 2 and len(segs) <= fk.INLINE_RUNS:
+                fk.flowkv_transfer_inline(src, dst, segs, len(S), stream=stream)
+            else:
+                dev = fk.segments_to_device(segs, src.device, stream)
+                keep.append(dev)
+                fk.flowkv_transfer(src, dst, dev, len(segs), len(S), stream=stream)
+        stream.synchronize()
+        return len(keep)
+
+    with ThreadPoolExecutor(4) as ex:
+        list(ex.map(worker, range(4)))
+    torch.cuda.synchronize()
+    for reqs in jobs:
+        for S, D in reqs:
+            oracle.transfer_fast(h_src, h_dst, S, D)
+    got = download_all(dst)
+    assert host_equal(got, h_dst), first_mismatch(got, h_dst)
 
 
 # ---- full-size workloads -----------------------------------------------------
