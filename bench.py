@@ -2,18 +2,22 @@
 
 Default workload: one Llama-3-8B-shape request of 13,000 tokens (813 blocks
 of 2 MiB: 32 layers x K/V x 16 tokens x 8 KV heads x 128 dims, bf16) moved
-between two 65,536-block pools.  A step is one pass of the whole hot path for
-that request:
-  1. the receiver's segment allocator places the request's 813 blocks in its
-     30%-occupied pool (host),
-  2. bidirectional segment alignment of the sender's and receiver's block
+between two 65,536-block pools.  The sender's blocks come from the segment
+allocator on a fresh pool (one run); the receiver's table comes from a seeded
+free list (free IDs ascending) of a pool with 30% of its blocks held at
+random, which gives 255 runs.  A step is one pass of the hot path for that
+request:
+  1. bidirectional segment alignment of the sender's and receiver's block
      lists (host),
-  3. the plan goes to the device: in the kernel's arguments when it has at
-     most 64 runs (it has 43), else staged through a ring of pinned buffers
-     (one small copy on a side stream, overlapping the previous kernel),
-  4. one kernel launch moves every run's K and V of all 32 layers,
-  5. the receiver's blocks are released again so every step sees the same
-     pool state (host bookkeeping, after the launch).
+  2. the plan goes to the device: in the kernel's arguments when it has at
+     most 64 runs, else staged through a ring of pinned buffers (one small
+     copy on a side stream, overlapping the previous kernel),
+  3. one kernel launch moves every run's K and V of all 32 layers.
+With --dst-policy segment the receiver's segment allocator also runs inside
+every step: it places the request's 813 blocks in the 30%-occupied pool (43
+runs, so the plan rides in the kernel's arguments) and releases them after
+the launch, so every step sees the same pool state.  The default run also
+times that receiver the same way and reports it under context.
 The other workloads (--workload) take their block lists from the allocators
 at setup, as their recipes describe; their step is plan + stage + one launch
 for the whole batch.  Steps are enqueued back to back on one stream; host work
@@ -85,8 +89,11 @@ def parse():
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="8b")
     ap.add_argument("--layout", choices=["block", "layer"], default="block",
                     help="pool layout of both sides: Eq. 5 block-major or per-layer")
-    ap.add_argument("--dst-policy", choices=["segment", "fifo_sorted"], default="segment",
-                    help="receiver allocator of the 8b workload")
+    ap.add_argument("--dst-policy", choices=["segment", "fifo_sorted", "fifo_shuffled"],
+                    default="fifo_sorted", help="receiver allocator of the 8b workload")
+    ap.add_argument("--dst-occupied", type=float, default=0.30,
+                    help="8b workload: fraction of the receiver's blocks held at random before "
+                         "the request arrives")
     ap.add_argument("--layerwise", action="store_true",
                     help="move each plan as one launch per layer (the paper's layer-wise "
                          "ablation) instead of one launch for all layers")
@@ -99,6 +106,9 @@ def parse():
     ap.add_argument("--unroll", type=int, default=0)
     ap.add_argument("--grid", type=int, default=0)
     ap.add_argument("--cache", type=int, default=0)
+    ap.add_argument("--order", type=int, default=0,
+                    help="tile visiting order: 1 plan order, 2 blocks scattered, 3 tiles "
+                         "scattered (0 = library default)")
     ap.add_argument("--attn-workload", choices=["batch", "8b", "70b"], default="batch",
                     help="attention: receiver pool and block lists of the batch (32 requests), "
                          "8b (one 13,000-token request) or 70b (the TP=8 share, 16 x 32,000 "
@@ -464,7 +474,10 @@ hipMemcpyDeviceToDeviceNoCU, one call per run, layer and K-or-V):
             for layer in range(geom.num_layers):
                 sdma_layer(layer, main_s)
         elif mode == "one_launch_after":
-            fk.flowkv_transfer_inline(src, dst, segs, n, stream=main_s)
+            if len(segs) <= fk.INLINE_RUNS:
+                fk.flowkv_transfer_inline(src, dst, segs, n, stream=main_s)
+            else:
+                fk.flowkv_transfer_ex(src, dst, segs_dev, len(segs), n, stream=main_s)
         elif mode == "layerwise_after":
             for layer in range(geom.num_layers):
                 fk.flowkv_transfer_layers(src, dst, segs_dev, len(segs), n, layer, 1,
@@ -600,7 +613,7 @@ def main():
     recipe, rargs, wl_desc = WORKLOADS[args.workload]
     shrunk = None
     if single:
-        wl = recipes.llama8b_13k(make_alloc, args.dst_policy)
+        wl = recipes.llama8b_13k(make_alloc, args.dst_policy, occupied=args.dst_occupied)
         # a device without room for both 65,536-block pools gets a smaller
         # receiver pool (the request's 813 blocks still fit at 30% occupancy)
         free, _ = torch.cuda.mem_get_info()
@@ -610,7 +623,8 @@ def main():
             shrunk = {"receiver_pool_blocks_from": wl.dst_pool_blocks, "to": fit,
                       "reason": f"{free / 2**30:.1f} GiB of device memory free"}
             print(f"receiver pool shrunk to {fit} blocks: {shrunk['reason']}", file=sys.stderr)
-            wl = recipes.llama8b_13k(make_alloc, args.dst_policy, dst_pool_blocks=fit)
+            wl = recipes.llama8b_13k(make_alloc, args.dst_policy, dst_pool_blocks=fit,
+                                     occupied=args.dst_occupied)
     elif recipe == "tiny":
         wl = recipes.tiny()
     else:
@@ -631,28 +645,44 @@ def main():
     dst = fk.KVPool(layout, make_device_pool(geom, layout, dst_blocks, dev, seed=1))
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t0
-    cfg = dict(threads=args.threads, unroll=args.unroll, grid=args.grid, cache=args.cache)
+    cfg = dict(threads=args.threads, unroll=args.unroll, grid=args.grid, cache=args.cache,
+               order=args.order)
     stream = torch.cuda.current_stream()
     stager = fk.PlanStager(dev, capacity=max(1, n))
 
+    def single_request_steps(policy):
+        """(make_plan, after_launch, receiver_list) of the 13k request for a
+        receiver policy.  The segment allocator runs inside every step on the
+        30%-occupied pool: the request's blocks are taken and released again,
+        and releasing merges them back, so every step sees the same state.  A
+        free list hands out other blocks after every release, so for it the
+        receiver's table is the one the seeded free list gave at setup (the
+        recipe's), planned and moved every step."""
+        if policy == "segment":
+            alloc = fk.Allocator(dst_blocks, POLICIES[policy], SEED_DST_TABLE)
+            alloc.mark_used(occupied_blocks(dst_blocks, args.dst_occupied, SEED_OCCUPANCY))
+
+            def plan_seg():
+                D = alloc.alloc(n)
+                return fk.flowkv_plan(S_all, D, src_blocks, dst_blocks), D
+
+            def release(D):
+                alloc.free(D)
+
+            def table():
+                D = alloc.alloc(n)
+                alloc.free(D)
+                return D
+            return plan_seg, release, table
+        D_fixed = D_all if policy == args.dst_policy else recipes.llama8b_13k(
+            make_alloc, policy, dst_pool_blocks=dst_blocks, occupied=args.dst_occupied).tables[0][1]
+
+        def plan_fixed():
+            return fk.flowkv_plan(S_all, D_fixed, src_blocks, dst_blocks), None
+        return plan_fixed, (lambda _: None), (lambda: D_fixed)
+
     if single:
-        # the receiver's allocator runs inside every step: same occupancy as the
-        # recipe, the request's blocks taken and released each step
-        dst_alloc = fk.Allocator(dst_blocks, POLICIES[args.dst_policy], SEED_DST_TABLE)
-        dst_alloc.mark_used(occupied_blocks(dst_blocks, 0.30, SEED_OCCUPANCY))
-
-        def make_plan():
-            D = dst_alloc.alloc(n)
-            segs = fk.flowkv_plan(S_all, D, src_blocks, dst_blocks)
-            return segs, D
-
-        def after_launch(D):
-            dst_alloc.free(D)
-
-        def receiver_list():
-            D = dst_alloc.alloc(n)
-            dst_alloc.free(D)
-            return D
+        make_plan, after_launch, receiver_list = single_request_steps(args.dst_policy)
     else:
         def make_plan():
             return fk.flowkv_plan_batch(offsets, S_all, D_all, src_blocks, dst_blocks), None
@@ -663,8 +693,9 @@ def main():
         def receiver_list():
             return D_all
 
-    def step(events=None):
-        segs, token = make_plan()
+    def step(events=None, fns=None):
+        plan_fn, release_fn = fns or (make_plan, after_launch)
+        segs, token = plan_fn()
         # small plans ride in the kernel arguments; longer ones are staged
         inline = len(segs) <= fk.INLINE_RUNS and not args.layerwise and not args.staged_plan
         segs_dev = None if inline else stager.stage(segs, stream)
@@ -682,21 +713,23 @@ def main():
             events[1].record(stream)
         if not inline:
             stager.release(stream)
-        after_launch(token)
+        release_fn(token)
         return segs
+
+    def spot_check(D_chk):
+        """A few moved blocks byte-equal (first, middle, last)."""
+        for i in sorted({0, n // 2, n - 1}):
+            if layout == fk.LAYOUT_BLOCK_MAJOR:
+                ok = torch.equal(src.tensors[0][int(S_all[i])], dst.tensors[0][int(D_chk[i])])
+            else:
+                ok = all(torch.equal(t_s[:, int(S_all[i])], t_d[:, int(D_chk[i])])
+                         for t_s, t_d in zip(src.tensors, dst.tensors))
+            assert ok, f"block {i} not moved"
 
     segs = step()
     torch.cuda.synchronize()
     n_runs = len(segs)
-    # spot check of the measured configuration: a few moved blocks byte-equal
-    D_chk = receiver_list()
-    for i in sorted({0, n // 2, n - 1}):
-        if layout == fk.LAYOUT_BLOCK_MAJOR:
-            ok = torch.equal(src.tensors[0][int(S_all[i])], dst.tensors[0][int(D_chk[i])])
-        else:
-            ok = all(torch.equal(t_s[:, int(S_all[i])], t_d[:, int(D_chk[i])])
-                     for t_s, t_d in zip(src.tensors, dst.tensors))
-        assert ok, f"block {i} not moved"
+    spot_check(receiver_list())
 
     for _ in range(args.warmup):
         step()
@@ -812,6 +845,37 @@ def main():
             torch.cuda.synchronize()
             context["per_run_copy_calls"] = calls
             context["per_run_copy_ms"] = round((time.perf_counter() - t_runs) * 1e3, 3)
+        # the other receiver policy, timed the same way in the same run (the
+        # segment allocator beside the seeded free list, or the reverse)
+        if single and not args.calibration_only and not args.layerwise:
+            alt = "segment" if args.dst_policy != "segment" else "fifo_sorted"
+            plan_alt, release_alt, table_alt = single_request_steps(alt)
+            fns = (plan_alt, release_alt)
+            segs_alt = step(fns=fns)
+            torch.cuda.synchronize()
+            spot_check(table_alt())
+            for _ in range(args.warmup):
+                step(fns=fns)
+            evs_alt = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                       for _ in range(args.steps)]
+            torch.cuda.synchronize()
+            gc.collect()
+            gc.disable()
+            t_alt = time.perf_counter()
+            for e in evs_alt:
+                step(e, fns=fns)
+            torch.cuda.synchronize()
+            el_alt = time.perf_counter() - t_alt
+            gc.enable()
+            k_alt = statistics.fmean(a.elapsed_time(b) for a, b in evs_alt)
+            context[f"receiver_{alt}"] = {
+                "runs": len(segs_alt),
+                "plan_in": ("kernel-arguments" if len(segs_alt) <= fk.INLINE_RUNS
+                            and not args.staged_plan else "device-memory"),
+                "kernel_ms_avg": round(k_alt, 4),
+                "roofline_frac": round((2 * payload + 16 * len(segs_alt)) / (k_alt * 1e-3) / 1e9
+                                       / HBM_PEAK_GBPS, 4),
+                "ms_per_step": round(el_alt * 1e3 / args.steps, 4)}
 
     # ---- CPU baseline: the oracle on the host ----------------------------------------
     cpu = None
@@ -872,7 +936,7 @@ def main():
               "pool_blocks": [src_blocks, dst_blocks], "layout": f"{args.layout}-major",
               "runs": n_runs}
     if single:
-        config.update(receiver_policy=args.dst_policy, receiver_occupied=0.30)
+        config.update(receiver_policy=args.dst_policy, receiver_occupied=args.dst_occupied)
         if shrunk:
             config["receiver_pool_shrunk"] = shrunk
     if args.layerwise:

@@ -86,20 +86,21 @@ def tiny() -> Workload:
 
 def llama8b_13k(make_alloc: MakeAlloc, dst_policy: str = "fifo_sorted",
                 pool_blocks: int = 65_536, tokens: int = 13_000,
-                dst_pool_blocks: int = 0) -> Workload:
+                dst_pool_blocks: int = 0, occupied: float = 0.30) -> Workload:
     """dst_pool_blocks (0: the same as pool_blocks) shrinks the receiver's
-    pool where a device cannot hold two full ones; it stays 30% occupied."""
+    pool where a device cannot hold two full ones; `occupied` is the
+    fraction of its blocks held at random before the request arrives."""
     g = LLAMA3_8B
     n = blocks_for(tokens, g.block_size)
     dst_blocks = dst_pool_blocks or pool_blocks
     src = make_alloc(pool_blocks, POLICY_SEGMENT, SEED_SRC_TABLE)
     S = np.asarray(src.alloc(n), dtype=np.int32)
     dst = make_alloc(dst_blocks, POLICIES[dst_policy], SEED_DST_TABLE)
-    dst.mark_used(occupied_blocks(dst_blocks, 0.30, SEED_OCCUPANCY))
+    dst.mark_used(occupied_blocks(dst_blocks, occupied, SEED_OCCUPANCY))
     D = np.asarray(dst.alloc(n), dtype=np.int32)
     return Workload(f"llama3-8b-13k/{dst_policy}", g, pool_blocks, dst_blocks, [(S, D)],
-                    [tokens], f"receiver pool of {dst_blocks} blocks 30% occupied, receiver "
-                              f"policy {dst_policy}")
+                    [tokens], f"receiver pool of {dst_blocks} blocks {occupied:.0%} occupied, "
+                              f"receiver policy {dst_policy}")
 
 
 def batch32(make_alloc: MakeAlloc, policy: str = "segment", id_space: int = 200_000,
