@@ -520,11 +520,13 @@ def segments_to_device(segs: np.ndarray, device, stream=None):
 class PlanStager:
     """Ring of pinned host and device buffers for plans.
 
-    ``stage(segs, stream)`` copies a plan to the device on a side stream and
-    makes ``stream`` wait for that copy, so the upload overlaps whatever
-    ``stream`` is still running; ``release(stream)`` marks the slot busy until
-    ``stream`` passes the kernel that reads it.  A slot is reused only after
-    that (the host waits), so at most ``slots`` plans are in flight."""
+    ``stage(segs, stream)`` copies a plan to the device.  While ``stream``
+    still runs earlier work, the copy goes on a side stream and ``stream``
+    waits for it, so the upload overlaps that work; on an idle stream it goes
+    on ``stream`` itself, which saves the cross-stream wait (about 35 us on
+    an MI355X).  ``release(stream)`` marks the slot busy until ``stream``
+    passes the kernel that reads it.  A slot is reused only after that (the
+    host waits), so at most ``slots`` plans are in flight."""
 
     def __init__(self, device, capacity: int = 4096, slots: int = 4):
         import torch
@@ -564,10 +566,14 @@ class PlanStager:
             self.done[j].synchronize()
         if k:
             self.host[j].numpy()[:k] = np.ascontiguousarray(segs).view(np.int32).reshape(-1, 4)
-            with torch.cuda.stream(self.copy_stream):
-                self.dev[j][:k].copy_(self.host[j][:k], non_blocking=True)
-                self.copied[j].record(self.copy_stream)
-            stream.wait_event(self.copied[j])
+            if stream.query():
+                with torch.cuda.stream(stream):
+                    self.dev[j][:k].copy_(self.host[j][:k], non_blocking=True)
+            else:
+                with torch.cuda.stream(self.copy_stream):
+                    self.dev[j][:k].copy_(self.host[j][:k], non_blocking=True)
+                    self.copied[j].record(self.copy_stream)
+                stream.wait_event(self.copied[j])
         self.used[j] = True
         return self.dev[j][:k]
 

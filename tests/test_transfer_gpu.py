@@ -163,6 +163,42 @@ def test_two_streams_two_plans():
     assert host_equal(download_all(dst), h_dst)
 
 
+def test_plan_stager_on_idle_and_busy_streams():
+    """PlanStager copies a plan on the stream itself when it is idle and on
+    its side stream behind running work; with more plans than ring slots and
+    one plan above the ring's capacity (the ring grows), every transfer
+    equals the oracle's."""
+    geom = Geometry("stager", 2, 2, 64, 16, "float16")      # 16 KiB blocks
+    B = 2048
+    src = device_pool(geom, BM, B, 0)
+    dst = device_pool(geom, BM, B, 1)
+    h_src, h_dst = download_all(src), download_all(dst)
+    stager = fk.PlanStager(src.device, capacity=8, slots=2)
+    stream = torch.cuda.current_stream()
+    filler = torch.empty(256 << 20, dtype=torch.uint8, device=src.device)
+    g = np.random.default_rng(9)
+    perm = g.permutation(B).astype(np.int32)
+    pos, seen = 0, set()
+    for i in range(12):
+        n = 300 if i == 7 else int(g.integers(1, 100))
+        S, D = g.permutation(B)[:n].astype(np.int32), perm[pos:pos + n]
+        pos += n
+        segs = fk.flowkv_plan(S, D, B, B)
+        if i % 3 == 0:
+            torch.cuda.synchronize()          # idle: the copy goes on the stream
+        else:
+            filler.fill_(i)                   # busy: the copy goes on the side stream
+        seen.add(stream.query())
+        dev = stager.stage(segs, stream)
+        fk.flowkv_transfer_ex(src, dst, dev, len(segs), n, stream=stream)
+        stager.release(stream)
+        oracle.transfer_fast(h_src, h_dst, S, D)
+    torch.cuda.synchronize()
+    assert seen == {True, False}
+    got = download_all(dst)
+    assert host_equal(got, h_dst), first_mismatch(got, h_dst)
+
+
 def test_launches_from_four_host_threads():
     """The launcher is reentrant: four host threads each plan and enqueue
     transfers on a stream of their own at the same time (ctypes releases the
