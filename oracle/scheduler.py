@@ -30,6 +30,20 @@ Status vector order (Algorithm 1):
     8 T_b     9 KV_u   10 G_u     11 MB_u        shared
 Weights per role, in the order of the score's terms:
     w_r, w_w, w_sw, w_se, w_t, w_kv, w_g, w_mb
+
+Parity: the steps Algorithm 1 states are pinned in
+``tests/test_oracle_scheduler.py``:
+- one-hot weights read the indicator each term names;
+- window closed forms (a constant passes through; a spike leaves after
+  exactly ``window`` samples; a ramp's mean);
+- averages over own-role nodes only;
+- hand-worked scenario boundaries, idle sets and the persistence of
+  extreme load;
+- routing against brute force over every (prefill, decode) pair.
+
+The readings themselves (window, normalisation, weights, thresholds, the
+TTFT and latency models, the idle node's new role) are **parity unpinned**:
+the paper prints no example or number to check them against.
 """
 
 from __future__ import annotations
