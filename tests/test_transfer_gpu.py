@@ -7,6 +7,7 @@ sample of the untouched receiver blocks with their pre-image.  Every case goes t
 (allocator, planner, transfer) via the ctypes binding.
 """
 
+import gc
 import itertools
 import sys
 
@@ -123,6 +124,25 @@ def test_last_block_ids_and_max_layers():
     tables = [(np.array([8, 0, 7], np.int32), np.array([6, 5, 0], np.int32))]
     for sl, dl in LAYOUT_PAIRS:
         check_full_pool(geom, sl, dl, Bs, Bd, tables)
+
+
+@pytest.mark.parametrize("path", ["per_lane", "uniform"])
+def test_blocks_just_under_the_2_gib_limit(path):
+    """The largest block the launcher accepts (2 x layers x H < 2 GiB), where
+    offsets inside a block use the top of 31 bits: one layer, H = 2^30 - 256
+    (not a multiple of the 16 KiB line: per-lane path) or 2^30 - 16,384
+    (uniform path); 3-block pools, both layouts."""
+    if path == "per_lane":
+        geom = Geometry("huge-lane", 1, 3, 128, 1398101, "bfloat16")    # H = 2^30 - 256
+    else:
+        geom = Geometry("huge-uni", 1, 64, 128, 65535, "bfloat16")      # H = 2^30 - 16384
+    assert 2**31 - 2**15 <= geom.block_bytes < 2**31
+    tables = [(np.array([2, 0], np.int32), np.array([1, 2], np.int32))]
+    for sl, dl in ((BM, BM), (LM, BM)):
+        say(f"{path}: block {geom.block_bytes} B, {NAMES[sl]}->{NAMES[dl]}")
+        check_full_pool(geom, sl, dl, 3, 3, tables)
+        gc.collect()
+        torch.cuda.empty_cache()
 
 
 def test_plan_records_outside_pools_are_skipped():
