@@ -120,6 +120,21 @@ def test_llama8b_geometry_long_requests(layout):
     say(f"  max error {err:.2e}")
 
 
+@pytest.mark.parametrize("layout", [BM, LM], ids=lambda x: NAMES[x])
+def test_blocks_beyond_4_gib_into_the_pool(layout):
+    """A 140,000-block pool of 8.5 GiB (one layer, 32 KiB chunks) with the
+    requests' blocks drawn at random from all of it: most K/V reads sit past
+    4 GiB from the pool's base (in the layer-major layout the V half starts
+    at 4.3 GiB), so block offsets must be formed in 64 bits."""
+    geom = Geometry("far", 1, 8, 128, 16, "bfloat16")
+    B = 140_000
+    assert B * geom.block_bytes > 2**32 and B * geom.chunk_bytes > 2**32
+    lens = [2000, 1500, 777]
+    say(f"far blocks {NAMES[layout]}: pool {B * geom.block_bytes / 2**30:.1f} GiB")
+    _, err = run_case(geom, layout, B, lens, 32, 31, layer=0)
+    say(f"  max error {err:.2e}")
+
+
 def test_llama70b_share_geometry():
     """One GPU's share of Llama-3-70B at TP=8: 1 KV head, 8 query heads."""
     geom = Geometry("llama70b-tp8", 80, 1, 128, 16, "bfloat16")
