@@ -64,8 +64,14 @@ def first_mismatch(a: oracle.HostPool, b: oracle.HostPool):
     return None
 
 
-def run_transfer(src, dst, segs, stream=None, **cfg):
+def run_transfer(src, dst, segs, stream=None, inline=False, **cfg):
+    """One launch of the plan: from device memory, or (inline) carried in
+    the kernel's arguments as bench.py sends plans of at most 64 runs."""
     total = fk.plan_total_blocks(segs)
+    if inline:
+        fk.flowkv_transfer_inline(src, dst, segs, total, stream=stream, **cfg)
+        torch.cuda.synchronize()
+        return None
     dev = fk.segments_to_device(segs, src.device) if len(segs) else torch.zeros(
         (0, 4), dtype=torch.int32, device=src.device)
     if cfg:
@@ -122,7 +128,7 @@ def moved_blocks_equal(src: fk.KVPool, dst: fk.KVPool, S, D) -> bool:
 
 
 def check_sampled(wl, wl_ref, sl, dl, max_blocks=1536, untouched_frac=0.01, max_untouched=1024,
-                  seed_sample=7, **cfg):
+                  seed_sample=7, inline=False, **cfg):
     """Full-size comparison: a seeded sample of the moved blocks (all of them
     when there are at most max_blocks) against the oracle; every moved block
     against its sender block on the device (`moved_blocks_equal`); and the
@@ -160,7 +166,7 @@ def check_sampled(wl, wl_ref, sl, dl, max_blocks=1536, untouched_frac=0.01, max_
     rest = rest[sample_indices(rest.size, k, seed_sample + 1)] if k else rest[:0]
     keep = np.unique(np.concatenate((guards[:max_untouched], rest))).astype(np.int64)
     before = download_blocks(dst, keep)
-    run_transfer(src, dst, segs, **cfg)
+    run_transfer(src, dst, segs, inline=inline, **cfg)
     # oracle on compact pools: sampled logical block i moves from compact
     # sender block i to compact receiver block i
     expect = oracle.HostPool.zeros(dl, geom.num_layers, len(pick), geom.block_size,

@@ -285,6 +285,17 @@ def test_llama8b_13k_full_size(policy, sl, dl):
     say(f"  {len(segs)} runs, {nb} blocks checked, {nk} untouched checked")
 
 
+@pytest.mark.parametrize("sl,dl", [(BM, BM), (LM, BM)], ids=lambda x: NAMES[x])
+def test_llama8b_13k_full_size_plan_in_kernel_arguments(sl, dl):
+    """The 13k request with the segment-allocator receiver (43 runs) in the
+    launch bench.py times for it: the plan carried in the kernel's
+    arguments."""
+    wl, ref = build(recipes.llama8b_13k, "segment")
+    segs, nb, nk = check_sampled(wl, ref, sl, dl, inline=True)
+    assert len(segs) <= fk.INLINE_RUNS and nb == 813
+    say(f"  inline: {len(segs)} runs, {nb} blocks checked, {nk} untouched checked")
+
+
 @pytest.mark.parametrize("policy", ["segment", "fifo_shuffled"])
 def test_batch32_full_size(policy):
     wl, ref = build(recipes.batch32, policy)
