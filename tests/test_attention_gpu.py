@@ -11,6 +11,7 @@ weight into P.V as two bfloat16 parts, hi + lo, which keep it to a relative
 |out - oracle| <= 2e-4 * max|V| + 1e-6.
 """
 
+import gc
 import sys
 
 import numpy as np
@@ -20,7 +21,7 @@ import torch
 import oracle
 from oracle.attention import decode_attention
 from paper_2504_03775_amd import flowkv as fk
-from workloads import Geometry, make_device_pool
+from workloads import Geometry, make_device_pool, recipes
 from tests.gpu_helpers import BM, LM, download_blocks
 
 pytestmark = pytest.mark.gpu
@@ -225,3 +226,77 @@ def test_blocks_outside_the_pool_contribute_nothing(layout):
     err = np.abs(got - want).max()
     assert np.all(np.isfinite(got))
     assert err <= 2e-4 * vmax + 1e-6, err
+
+
+# ---- the bench's attention workloads at full size ------------------------------
+
+def download_layer(pool: fk.KVPool, ids, layer: int) -> oracle.HostPool:
+    """K and V of one layer of blocks `ids` of a block-major device pool, as a
+    compact one-layer block-major host pool (block i = block ids[i])."""
+    idx = torch.as_tensor(np.asarray(ids, dtype=np.int64), device=pool.device)
+    slot = pool.kv_heads * pool.head_dim * pool.elem_bytes
+    hp = oracle.HostPool.zeros(BM, 1, len(ids), pool.block_size, slot)
+    out = hp.buffers[0].reshape(len(ids), -1)
+    for lo in range(0, len(ids), 4096):
+        sub = pool.tensors[0].index_select(0, idx[lo:lo + 4096])[:, layer].contiguous()
+        out[lo:lo + 4096] = sub.view(torch.uint8).reshape(sub.shape[0], -1).cpu().numpy()
+    return hp
+
+
+BENCH_ATTN = {  # as bench.py --op attention builds them: recipe, query heads
+    "batch": (lambda mk: recipes.batch32(mk, "segment"), 32),
+    "8b": (lambda mk: recipes.llama8b_13k(mk, "segment"), 32),
+    "70b": (lambda mk: recipes.llama70b_tp8(mk, "segment"), 8),
+}
+
+
+@pytest.mark.parametrize("name", sorted(BENCH_ATTN))
+def test_bench_attention_workloads_full_size(name):
+    """Each --op attention workload exactly as bench.py runs it: its recipe's
+    block lists, the full receiver pool (block-major, seeded N(0,1)), every
+    request in one call, the default split, the middle layer; the outputs of
+    a sample of requests (shortest, longest and two between) against the
+    oracle on just those requests' blocks of that layer."""
+    make, q_heads = BENCH_ATTN[name]
+    wl = make(lambda P, pol, seed: fk.Allocator(P, pol, seed))
+    geom = wl.geom
+    gc.collect()
+    torch.cuda.empty_cache()
+    pool = fk.KVPool(BM, make_device_pool(geom, BM, wl.dst_pool_blocks, "cuda", 1))
+    lens = np.asarray(wl.tokens, dtype=np.int32)
+    n, max_seq = len(lens), int(lens.max())
+    max_blocks = max(len(d) for _, d in wl.tables)
+    tab = np.full((n, max_blocks), -1, dtype=np.int32)
+    for r, (_, d) in enumerate(wl.tables):
+        tab[r, :len(d)] = d
+    q = torch.randn((n, q_heads, geom.head_dim), generator=torch.Generator("cuda").manual_seed(3),
+                    device="cuda").to(torch.bfloat16)
+    layer, scale = geom.num_layers // 2, 1.0 / geom.head_dim ** 0.5
+    ws = torch.empty(fk.flowkv_decode_attention_workspace(n, q_heads, geom.head_dim, max_seq),
+                     dtype=torch.uint8, device="cuda")
+    out = torch.full((n, q_heads, geom.head_dim), float("nan"), dtype=torch.float32, device="cuda")
+    fk.flowkv_decode_attention(pool, layer, q, torch.as_tensor(tab, device="cuda"),
+                               torch.as_tensor(lens, device="cuda"), max_seq, scale, out, ws)
+    torch.cuda.synchronize()
+    order = np.argsort(lens, kind="stable")
+    pick = sorted({int(order[0]), int(order[-1]), int(order[n // 3]), int(order[(2 * n) // 3])})
+    say(f"{name}: {n} requests, {int(lens.sum())} tokens, pool {wl.dst_pool_blocks} blocks, "
+        f"split {fk.flowkv_decode_attention_split(n, max_seq)}; checking requests {pick}")
+    got = out.cpu().numpy().astype(np.float64)
+    assert np.all(np.isfinite(got))
+    ids = np.concatenate([wl.tables[r][1] for r in pick]).astype(np.int64)
+    host = download_layer(pool, ids, layer)
+    ctabs, pos = [], 0
+    for r in pick:
+        k = len(wl.tables[r][1])
+        ctabs.append(list(range(pos, pos + k)))
+        pos += k
+    want = decode_attention(host, bf16_to_f64(q[pick]), ctabs, [int(lens[r]) for r in pick], 0,
+                            geom.kv_heads, geom.head_dim, scale)
+    vmax = float(pool.tensors[0][:, layer].abs().max())
+    err = np.abs(got[pick] - want).max()
+    tol = 2e-4 * vmax + 1e-6
+    say(f"  max error {err:.2e} (tolerance {tol:.2e})")
+    assert err <= tol
+    del pool
+    torch.cuda.empty_cache()
