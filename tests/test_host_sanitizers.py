@@ -27,9 +27,11 @@ def test_host_code_under_asan_and_ubsan(tmp_path):
            os.path.join(ROOT, "tests", "native", "host_check.cpp"),
            *[os.path.join(CSRC, s) for s in HOST_SOURCES], "-o", exe]
     subprocess.run(cmd, check=True, capture_output=True, timeout=300)
-    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:abort_on_error=0",
+    # verify_asan_link_order=0: the sanitizer runtime need not be the first
+    # library loaded, so the process environment is passed on unchanged
+    env = dict(os.environ,
+               ASAN_OPTIONS="detect_leaks=1:abort_on_error=0:verify_asan_link_order=0",
                UBSAN_OPTIONS="print_stacktrace=1:halt_on_error=1")
-    env.pop("LD_PRELOAD", None)
     r = subprocess.run([exe, "150"], capture_output=True, text=True, timeout=600, env=env)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "rounds ok" in r.stdout
