@@ -2,7 +2,10 @@
 
 ``python -m paper_2504_03775_amd.build`` compiles the host C++ (allocator,
 planner, scheduler, status) with g++ and the HIP translation unit (kernel + launcher)
-with hipcc, then links them into ``paper_2504_03775_amd/libflowkv.so``.
+with hipcc, then links them into ``paper_2504_03775_amd/libflowkv.so``.  In a
+checkout with ``tests/native/abi_transfer.cpp`` it also builds that program,
+which drives the library through the C ABI alone (no Python), next to its
+source.
 """
 
 from __future__ import annotations
@@ -63,7 +66,25 @@ def build(verbose: bool = True, extra_host_flags=(), lib_path: str = LIB,
     _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *extra_host_flags, *objs,
           "-o", tmp], verbose)
     os.replace(tmp, lib_path)
+    if lib_path == LIB:
+        build_abi_check(verbose)
     return lib_path
+
+
+def build_abi_check(verbose: bool = True):
+    """tests/native/abi_transfer: host C++ against include/flowkv.h and the
+    HIP runtime API, linked to the in-tree library (found through its rpath)."""
+    src = os.path.join(ROOT, "tests", "native", "abi_transfer.cpp")
+    if not os.path.exists(src):
+        return None
+    exe = src[:-len(".cpp")]
+    rocm = os.path.dirname(os.path.dirname(os.path.realpath(_hipcc())))
+    _run(["g++", "-O2", "-std=c++17", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
+          "-I", INCLUDE, "-I", os.path.join(rocm, "include"), src,
+          "-L", PKG, "-lflowkv", "-L", os.path.join(rocm, "lib"), "-lamdhip64",
+          "-Wl,-rpath,$ORIGIN/../../paper_2504_03775_amd",
+          f"-Wl,-rpath,{os.path.join(rocm, 'lib')}", "-o", exe], verbose)
+    return exe
 
 
 if __name__ == "__main__":

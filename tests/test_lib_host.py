@@ -345,6 +345,17 @@ def test_transfer_rejects_bad_pools_without_touching_the_device():
     assert xfer(good_src, good_dst, n_segs=-1) == fk.EINVAL
 
 
+def test_abi_check_program_is_built_and_runs_without_python():
+    """The build step also builds tests/native/abi_transfer, which uses the
+    library through the C ABI alone; its dynamic links resolve, and without
+    arguments it prints its usage (before any HIP call)."""
+    import subprocess
+    exe = os.path.join(os.path.dirname(os.path.abspath(__file__)), "native", "abi_transfer")
+    assert os.path.exists(exe), "run the build step first"
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 2 and "usage: abi_transfer" in r.stderr
+
+
 def test_binding_shares_torchs_hip_runtime():
     """Device pointers and streams come from torch, so the library must bind
     to torch's HIP runtime: exactly one libamdhip64 may be mapped."""
