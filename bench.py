@@ -280,8 +280,8 @@ def bench_attention(args):
 
 def attention_cpu_baseline(pool, geom, layer, q, wl, lens, scale, np, torch):
     """The float64 oracle on the host, on a bounded sample: the workload's
-    shortest request (its blocks downloaded to a compact host pool), timed
-    once; reported as K/V bytes read per second."""
+    shortest request (its blocks downloaded to a compact host pool), run
+    repeatedly for about 10 s; reported as K/V bytes read per second."""
     import oracle
     from oracle.attention import decode_attention
 
@@ -299,15 +299,18 @@ def attention_cpu_baseline(pool, geom, layer, q, wl, lens, scale, np, torch):
             hp.buffers[l_][:] = t.index_select(1, idx).contiguous().view(torch.uint8).cpu() \
                 .numpy().reshape(-1)
     qh = q[r:r + 1].float().cpu().numpy().astype(np.float64)
-    t0 = time.perf_counter()
-    decode_attention(hp, qh, [list(range(len(ids)))], [T], layer, geom.kv_heads,
-                     geom.head_dim, scale)
-    dt = time.perf_counter() - t0
+    reps, dt = 0, 0.0
+    while dt < 10.0 and reps < 1000:
+        t0 = time.perf_counter()
+        decode_attention(hp, qh, [list(range(len(ids)))], [T], layer, geom.kv_heads,
+                         geom.head_dim, scale)
+        dt += time.perf_counter() - t0
+        reps += 1
     kv = T * 2 * geom.kv_heads * geom.head_dim * 2
-    return {"value": round(kv / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+    return {"value": round(kv * reps / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"request {r} of the workload ({T} tokens, {kv} K/V bytes), one layer, "
-                      f"float64 numpy with a per-slot gather, one thread; "
-                      f"{os.cpu_count()} host cores visible"}
+                      f"repeated {reps}x ({dt:.1f} s), float64 numpy with a per-slot gather, "
+                      f"one thread; {os.cpu_count()} host cores visible"}
 
 
 def bench_schedule(args):
@@ -353,16 +356,18 @@ def bench_schedule(args):
     if not args.no_cpu_baseline:
         from oracle.scheduler import Params, RefScheduler
         ref = RefScheduler(Params(window, STATUS_SCALE, w, w, 0.5, 0.5, 1.0, 1.0, 0.1, 3), roles)
-        k = 3
-        as_lists = [s_.tolist() for s_ in samples[:k]]
-        t0 = time.perf_counter()
-        for i in range(k):
-            ref.observe(as_lists[i])
+        as_lists = [s_.tolist() for s_ in samples]
+        k, t_sum = 0, 0.0
+        while t_sum < 10.0 and k < 10_000:        # about 10 s of host work
+            t0 = time.perf_counter()
+            ref.observe(as_lists[k % len(as_lists)])
             ref.evaluate()
-        t_ref = (time.perf_counter() - t0) / k
+            t_sum += time.perf_counter() - t0
+            k += 1
+        t_ref = t_sum / k
         cpu = {"value": round(1.0 / t_ref, 2), "unit": "evaluations/s", "cores": 1,
                "kind": "oracle", "sample": f"{k} evaluations at {n} nodes, window {window}, "
-                                          "pure Python"}
+                                          f"pure Python ({t_sum:.1f} s)"}
 
     mixes = {"balanced": Workload(6.0, 400, [1000, 5000, 10000], [256], seed=1),
              "prefill-heavy": Workload(5.0, 300, [12000, 16000, 20000], [32], seed=2),
@@ -897,7 +902,7 @@ def main():
                     .reshape(-1).cpu().numpy()
         h_dst = oracle.HostPool.zeros(layout, geom.num_layers, k, geom.block_size, slot)
         reps, t_cpu = 0, 0.0
-        while t_cpu < 10.0 and reps < 20:
+        while t_cpu < 10.0 and reps < 100:
             t1 = time.perf_counter()
             oracle.transfer_fast(h_src, h_dst, np.arange(k), np.arange(k))
             t_cpu += time.perf_counter() - t1
@@ -910,7 +915,7 @@ def main():
         ids = np.arange(k)
         with ThreadPoolExecutor(threads) as ex:
             reps_m, t_m = 0, 0.0
-            while t_m < 5.0 and reps_m < 20:
+            while t_m < 5.0 and reps_m < 200:
                 t1 = time.perf_counter()
                 list(ex.map(lambda l: oracle.transfer_fast(h_src, h_dst, ids, ids, layers=[l]),
                             range(geom.num_layers)))
