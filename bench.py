@@ -83,7 +83,9 @@ def parse():
                     help="transfer: the KV transfer hot path (default); attention: one decode "
                          "step of paged attention over the receiver pool of the batch workload; "
                          "schedule: the load-aware scheduler (host) at 1,024 nodes, and the "
-                         "cluster model's three load mixes with fixed and load-aware roles")
+                         "cluster model's three load mixes with fixed and load-aware roles; "
+                         "overlap: the 13k request's transfer after, or layer by layer beside, "
+                         "a prefill stand-in")
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="8b")
@@ -126,14 +128,19 @@ def kernel_hash(src: str = KERNEL_SRC) -> str:
     return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
 
 
-def traffic_from_profile(summary: str = PMC_SUMMARY, src: str = KERNEL_SRC, split=None):
+def traffic_from_profile(summary: str = PMC_SUMMARY, src: str = KERNEL_SRC, split=None,
+                         runs=None):
     """HBM bytes per launch from the committed counter summary, scaled by the
     plain-copy calibration recorded with it; None if absent, if the kernel
-    source changed since the counters were taken, or (attention) if they were
-    taken at another split length."""
+    source changed since the counters were taken, or if they were taken on
+    another plan (run count) or (attention) at another split length."""
     if not summary or not os.path.exists(summary):
         return None
     text = open(summary).read()
+    if runs is not None:
+        mr = re.search(r"(\d+) runs x 16 B plan", text)
+        if not mr or int(mr.group(1)) != runs:
+            return None
     if split is not None:
         ms = re.search(r"split_tokens:\s*(\d+)", text)
         if not ms or int(ms.group(1)) != split:
@@ -932,8 +939,8 @@ def main():
                                           f"threads, repeated {reps_m}x"}}
         del h_src, h_dst
 
-    traffic = traffic_from_profile() if (single and args.layout == "block"
-                                         and not args.layerwise) else None
+    traffic = traffic_from_profile(runs=n_runs) if (single and args.layout == "block"
+                                                   and not args.layerwise) else None
     kv_dtype = {"bfloat16": "bf16", "float16": "fp16"}[geom.dtype]
     config = {"workload": wl_desc, "layers": geom.num_layers, "kv_heads": geom.kv_heads,
               "head_dim": geom.head_dim, "block_size": geom.block_size, "kv_dtype": kv_dtype,
