@@ -78,6 +78,29 @@ def test_receiver_pool_shrinks_to_fit():
     assert len(D) == 813 and D.max() < 36864 and len(set(D.tolist())) == 813
 
 
+def test_traffic_is_reported_only_for_the_profiled_kernel_and_plan(tmp_path):
+    """roofline.traffic comes from a committed counter summary only while the
+    kernel source hash, the plan's run count and (attention) the split length
+    match what the counters were taken on."""
+    import bench
+
+    src = tmp_path / "k.hip"
+    src.write_text("kernel v1")
+    h = bench.kernel_hash(str(src))
+    summ = tmp_path / "pmc.txt"
+    summ.write_text(f"algorithmic bytes: ... (payload 1, 255 runs x 16 B plan)\n"
+                    f"split_tokens: 1024\nhbm_bytes_per_launch: 3410881152\n"
+                    f"kernel_source_sha256_16: {h}\n")
+    f = bench.traffic_from_profile
+    assert f(str(summ), str(src)) == 3410881152.0
+    assert f(str(summ), str(src), runs=255, split=1024) == 3410881152.0
+    assert f(str(summ), str(src), runs=43) is None
+    assert f(str(summ), str(src), split=256) is None
+    assert f(str(tmp_path / "absent.txt"), str(src)) is None
+    src.write_text("kernel v2")
+    assert f(str(summ), str(src)) is None
+
+
 def test_schedule_line_contract_on_cpu():
     """bench.py --op schedule runs on the host alone: one JSON line with the
     scheduler's rate, the oracle beside it and the cluster model's mixes."""
