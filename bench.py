@@ -486,7 +486,7 @@ hipMemcpyDeviceToDeviceNoCU, one call per run, layer and K-or-V):
             for layer in range(geom.num_layers):
                 sdma_layer(layer, main_s)
         elif mode == "one_launch_after":
-            if len(segs) <= fk.INLINE_RUNS:
+            if len(segs) <= fk.inline_capacity(src, dst):
                 fk.flowkv_transfer_inline(src, dst, segs, n, stream=main_s)
             else:
                 fk.flowkv_transfer_ex(src, dst, segs_dev, len(segs), n, stream=main_s)
@@ -709,7 +709,8 @@ def main():
         plan_fn, release_fn = fns or (make_plan, after_launch)
         segs, token = plan_fn()
         # small plans ride in the kernel arguments; longer ones are staged
-        inline = len(segs) <= fk.INLINE_RUNS and not args.layerwise and not args.staged_plan
+        inline = (len(segs) <= fk.inline_capacity(src, dst) and not args.layerwise
+                  and not args.staged_plan)
         segs_dev = None if inline else stager.stage(segs, stream)
         if events is not None:
             events[0].record(stream)
@@ -882,7 +883,7 @@ def main():
             k_alt = statistics.fmean(a.elapsed_time(b) for a, b in evs_alt)
             context[f"receiver_{alt}"] = {
                 "runs": len(segs_alt),
-                "plan_in": ("kernel-arguments" if len(segs_alt) <= fk.INLINE_RUNS
+                "plan_in": ("kernel-arguments" if len(segs_alt) <= fk.inline_capacity(src, dst)
                             and not args.staged_plan else "device-memory"),
                 "kernel_ms_avg": round(k_alt, 4),
                 "roofline_frac": round((2 * payload + 16 * len(segs_alt)) / (k_alt * 1e-3) / 1e9
@@ -953,8 +954,8 @@ def main():
             config["receiver_pool_shrunk"] = shrunk
     if args.layerwise:
         config.update(launches_per_step=geom.num_layers, mode="layer-wise")
-    config["plan_in"] = ("kernel-arguments" if n_runs <= fk.INLINE_RUNS and not args.layerwise
-                         and not args.staged_plan else "device-memory")
+    config["plan_in"] = ("kernel-arguments" if n_runs <= fk.inline_capacity(src, dst)
+                         and not args.layerwise and not args.staged_plan else "device-memory")
     line = {
         "metric": METRIC,
         "value": round(value, 2),

@@ -88,6 +88,8 @@ enum {
 
 #define FLOWKV_MAX_LAYERS 128
 #define FLOWKV_INLINE_RUNS 64 /* plan records flowkv_transfer_inline carries */
+#define FLOWKV_INLINE_RUNS_BLOCK_MAJOR 300 /* ... between two block-major pools, as
+                                              the planner writes them */
 
 typedef struct flowkv_allocator flowkv_allocator; /* opaque, host memory only */
 
@@ -227,13 +229,17 @@ int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst,
                        int64_t total_blocks, const flowkv_launch_config* cfg,
                        void* hip_stream);
 
-/* flowkv_transfer_ex for small plans held in host memory: the records
-   (at most FLOWKV_INLINE_RUNS) are copied into the kernel's arguments at
-   launch, so the plan needs no device buffer and no separate host-to-device
-   copy; segs_host may be reused as soon as the call returns.  Same result as
-   flowkv_transfer_ex with the same plan in device memory.  ECAP when n_segs
-   exceeds FLOWKV_INLINE_RUNS (use flowkv_transfer_ex with a device plan);
-   other arguments and errors as for flowkv_transfer_ex. */
+/* flowkv_transfer_ex for small plans held in host memory: the records are
+   copied into the kernel's arguments at launch, so the plan needs no device
+   buffer and no separate host-to-device copy; segs_host may be reused as
+   soon as the call returns.  Same result as flowkv_transfer_ex with the same
+   plan in device memory.  Up to FLOWKV_INLINE_RUNS records fit; between two
+   block-major pools up to FLOWKV_INLINE_RUNS_BLOCK_MAJOR, provided the plan
+   is in the planner's form (record i starts where record i - 1 ends, every
+   record holds a block, and they cover [0, total_blocks)), since they then
+   travel as 12-byte records whose lengths follow from the next `first`.
+   ECAP otherwise (use flowkv_transfer_ex with a device plan); other
+   arguments and errors as for flowkv_transfer_ex. */
 int flowkv_transfer_inline(const flowkv_pool* src, const flowkv_pool* dst,
                            const flowkv_segment* segs_host, int64_t n_segs,
                            int64_t total_blocks, const flowkv_launch_config* cfg,

@@ -52,9 +52,8 @@ struct PoolArg {
 // Plans of up to kInlineRuns records can travel inside the kernel arguments.
 constexpr int kInlineRuns = FLOWKV_INLINE_RUNS;
 
-struct XferArgs {
-  PoolArg src;
-  PoolArg dst;
+// The launch's geometry and plan size, common to both argument forms.
+struct XferShape {
   const flowkv_segment* segs;
   int64_t chunk_bytes;      // H (bytes of one block/layer/K-or-V slab)
   int64_t block_bytes;      // BB = 2 * L * H (block stride of a block-major pool)
@@ -72,9 +71,40 @@ struct XferArgs {
   uint32_t h_shift;
   int32_t order;            // 1 plan order, 2 blocks scattered, 3 tiles scattered
   int64_t perm_mul;         // multiplier of the scattering permutation
+};
+
+struct XferArgs : XferShape {
+  PoolArg src;
+  PoolArg dst;
   flowkv_segment inline_runs[kInlineRuns];  // the plan, when it rides in the arguments
 };
-static_assert(sizeof(XferArgs) <= 4096, "kernel arguments must stay within 4 KiB");
+// The compiler appends 256 bytes of implicit arguments to every kernel's
+// argument segment; the whole segment stays within 4 KiB.
+constexpr size_t kImplicitArgBytes = 256;
+static_assert(sizeof(XferArgs) + kImplicitArgBytes <= 4096,
+              "kernel arguments must stay within 4 KiB");
+
+// Block-major pools on both sides need one base pointer each, which leaves
+// the kernel arguments room for longer plans in the planner's contiguous
+// form: 12-byte records, a run's length being the next record's `first`
+// minus its own (total_blocks for the last).
+struct CompactRun {
+  int32_t src_block, dst_block, first;
+};
+constexpr int kInlineRunsBM = FLOWKV_INLINE_RUNS_BLOCK_MAJOR;
+
+struct PoolArgBM {
+  char* base[1];
+  int64_t num_blocks;
+};
+
+struct XferArgsBM : XferShape {
+  PoolArgBM src;
+  PoolArgBM dst;
+  CompactRun inline_runs[kInlineRunsBM];
+};
+static_assert(sizeof(XferArgsBM) + kImplicitArgBytes <= 4096,
+              "kernel arguments must stay within 4 KiB");
 
 // Pool memory is global memory; naming the address space lets the compiler
 // emit global (not flat) vector loads and stores with a scalar base.
@@ -109,8 +139,8 @@ __device__ __forceinline__ void store16(gvec* p, u32x4 v) {
 // Start of line j (0 <= j < lines_per_block) of the moved span of block b
 // when every line lies in one chunk: chunk r = j / lines_per_chunk (counted
 // from layer0), line w = j % lines_per_chunk.
-template <bool kLM>
-__device__ __forceinline__ char* line_base(const PoolArg& p, const XferArgs& a, int64_t b,
+template <bool kLM, class P, class A>
+__device__ __forceinline__ char* line_base(const P& p, const A& a, int64_t b,
                                            int32_t j, int32_t r, int32_t w, int64_t line) {
   if constexpr (kLM)
     return p.base[a.layer0 + (r >> 1)] + (int64_t(r & 1) * p.num_blocks + b) * a.chunk_bytes +
@@ -121,8 +151,8 @@ __device__ __forceinline__ char* line_base(const PoolArg& p, const XferArgs& a, 
 
 // Tile t of a block when every line lies inside one chunk: all pointer
 // arithmetic is uniform across the workgroup; each lane adds its 16 bytes.
-template <bool kSrcLM, bool kDstLM, int kU, int kCache>
-__device__ __forceinline__ void copy_tile_uniform(const XferArgs& a, int64_t sb, int64_t db,
+template <bool kSrcLM, bool kDstLM, int kU, int kCache, class A>
+__device__ __forceinline__ void copy_tile_uniform(const A& a, int64_t sb, int64_t db,
                                                   int32_t t, int tid, int64_t line) {
   const int32_t j0 = t * kU;
   int32_t r = j0 / a.lines_per_chunk;
@@ -182,9 +212,9 @@ __device__ __forceinline__ uint32_t div_by_h(uint32_t o, uint32_t magic, uint32_
 
 // Byte o of the moved span of block b for any H (a multiple of 16): chunk
 // r = o / H, counted from layer0.
-template <bool kLM>
-__device__ __forceinline__ char* byte_addr(const PoolArg& p, char* const* lds_base,
-                                           const XferArgs& a, int64_t b, int64_t o) {
+template <bool kLM, class P, class A>
+__device__ __forceinline__ char* byte_addr(const P& p, char* const* lds_base,
+                                           const A& a, int64_t b, int64_t o) {
   if constexpr (kLM) {
     const uint32_t r = div_by_h(uint32_t(o), a.h_magic, a.h_shift);
     const int64_t w = o - int64_t(r) * a.chunk_bytes;
@@ -195,8 +225,8 @@ __device__ __forceinline__ char* byte_addr(const PoolArg& p, char* const* lds_ba
 }
 
 // Tile t of a block for any H: each lane finds its own chunk.
-template <bool kSrcLM, bool kDstLM, int kU, int kCache>
-__device__ __forceinline__ void copy_tile_lanes(const XferArgs& a, char* const* s_src,
+template <bool kSrcLM, bool kDstLM, int kU, int kCache, class A>
+__device__ __forceinline__ void copy_tile_lanes(const A& a, char* const* s_src,
                                                 char* const* s_dst, int64_t sb, int64_t db,
                                                 int32_t t, int tid, int64_t line) {
   const int64_t o0 = int64_t(t) * kU * line + int64_t(tid) * 16;
@@ -236,11 +266,25 @@ __device__ __forceinline__ flowkv_segment run_at(const XferArgs& a, const cseg* 
   else return load_seg(segs + i);
 }
 
+// The compact inline form: the same records, each run ending where the next
+// one starts.
+template <bool kInline>
+__device__ __forceinline__ int32_t run_first(const XferArgsBM& a, const cseg*, int32_t i) {
+  return a.inline_runs[i].first;
+}
+
+template <bool kInline>
+__device__ __forceinline__ flowkv_segment run_at(const XferArgsBM& a, const cseg*, int32_t i) {
+  const CompactRun r = a.inline_runs[i];
+  const int32_t end = i + 1 < a.n_segs ? a.inline_runs[i + 1].first : int32_t(a.total_blocks);
+  return flowkv_segment{r.src_block, r.dst_block, end - r.first, r.first};
+}
+
 // Index of the last run whose first block is <= g, by galloping from run s
 // (backward or forward) to a bracket [lo, hi) with first[lo] <= g < first[hi]
 // and bisecting it.  Always returns an index in [0, n).
-template <bool kInline>
-__device__ __forceinline__ int32_t find_run(const XferArgs& a, const cseg* segs, int32_t n,
+template <bool kInline, class A>
+__device__ __forceinline__ int32_t find_run(const A& a, const cseg* segs, int32_t n,
                                             int64_t g, int32_t s) {
   int32_t lo, hi, step = 1;
   if (run_first<kInline>(a, segs, s) > g) {
@@ -270,13 +314,15 @@ __device__ __forceinline__ int32_t find_run(const XferArgs& a, const cseg* segs,
 }
 
 // Where block g would sit if every run had the same length.
-__device__ __forceinline__ int32_t guess_run(const XferArgs& a, int64_t g) {
+template <class A>
+__device__ __forceinline__ int32_t guess_run(const A& a, int64_t g) {
   const int64_t s = g * a.n_segs / a.total_blocks;
   return int32_t(s < a.n_segs ? s : a.n_segs - 1);
 }
 
-template <bool kSrcLM, bool kDstLM, int kU, int kCache, bool kUniform, bool kInline>
-__global__ __launch_bounds__(1024) void kv_segment_copy(const XferArgs a) {
+template <bool kSrcLM, bool kDstLM, int kU, int kCache, bool kUniform, bool kInline,
+          class A = XferArgs>
+__global__ __launch_bounds__(1024) void kv_segment_copy(const A a) {
   __shared__ char* s_src[kUniform ? 1 : FLOWKV_MAX_LAYERS];
   __shared__ char* s_dst[kUniform ? 1 : FLOWKV_MAX_LAYERS];
   const int tid = threadIdx.x;
@@ -380,6 +426,45 @@ KernelFn pick_layouts(bool src_lm, bool dst_lm, int unroll, int cache, bool unif
 KernelFn pick_kernel(bool src_lm, bool dst_lm, int unroll, int cache, bool uniform, bool inl) {
   return inl ? pick_layouts<true>(src_lm, dst_lm, unroll, cache, uniform)
              : pick_layouts<false>(src_lm, dst_lm, unroll, cache, uniform);
+}
+
+// The compact inline form (block-major pools on both sides).
+using KernelFnBM = void (*)(XferArgsBM);
+
+template <int U, int C>
+KernelFnBM pick_bm_path(bool uniform) {
+  return uniform ? kv_segment_copy<false, false, U, C, true, true, XferArgsBM>
+                 : kv_segment_copy<false, false, U, C, false, true, XferArgsBM>;
+}
+
+template <int U>
+KernelFnBM pick_bm_cache(int cache, bool uniform) {
+  switch (cache) {
+    case 0: return pick_bm_path<U, 0>(uniform);
+    case 1: return pick_bm_path<U, 1>(uniform);
+    case 2: return pick_bm_path<U, 2>(uniform);
+    default: return pick_bm_path<U, 3>(uniform);
+  }
+}
+
+KernelFnBM pick_kernel_bm(int unroll, int cache, bool uniform) {
+  switch (unroll) {
+    case 2: return pick_bm_cache<2>(cache, uniform);
+    case 4: return pick_bm_cache<4>(cache, uniform);
+    case 8: return pick_bm_cache<8>(cache, uniform);
+    default: return pick_bm_cache<16>(cache, uniform);
+  }
+}
+
+// True when the records are the planner's form: run i starts where run i-1
+// ends, every run holds a block, and the runs cover [0, total_blocks).
+bool contiguous_plan(const flowkv_segment* r, int64_t n, int64_t total_blocks) {
+  int64_t next = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    if (r[i].first != next || r[i].n_blocks < 1) return false;
+    next += r[i].n_blocks;
+  }
+  return next == total_blocks;
 }
 
 // Library defaults, from interleaved launch-shape comparisons over the five
@@ -510,9 +595,25 @@ int launch_transfer(const flowkv_pool* src, const flowkv_pool* dst,
   if (cache < 1 || cache > 4) return fail(FLOWKV_EINVAL, "cache %d: need 1..4", cache);
   if (grid < 0) return fail(FLOWKV_EINVAL, "negative grid %d", grid);
   const bool inl = segs_host != nullptr;
-  if (inl && n_segs > kInlineRuns)
-    return fail(FLOWKV_ECAP, "%lld runs, at most %d travel in the kernel arguments",
-                (long long)n_segs, kInlineRuns);
+  // more than kInlineRuns records ride in the kernel arguments only in the
+  // compact form: block-major pools on both sides, the planner's records
+  bool compact = false;
+  if (inl && n_segs > kInlineRuns) {
+    const bool both_bm = src->layout == FLOWKV_LAYOUT_BLOCK_MAJOR &&
+                         dst->layout == FLOWKV_LAYOUT_BLOCK_MAJOR;
+    if (!both_bm || n_segs > kInlineRunsBM)
+      return fail(FLOWKV_ECAP,
+                  "%lld runs: at most %d travel in the kernel arguments (%d between "
+                  "block-major pools)",
+                  (long long)n_segs, kInlineRuns, kInlineRunsBM);
+    if (!contiguous_plan(segs_host, n_segs, total_blocks))
+      return fail(FLOWKV_ECAP,
+                  "%lld runs: beyond %d, a plan travels in the kernel arguments only as the "
+                  "planner writes it (each run starting where the previous one ends, the runs "
+                  "covering total_blocks)",
+                  (long long)n_segs, kInlineRuns);
+    compact = true;
+  }
   if (n_segs == 0 || total_blocks == 0 || layer_count == 0) return ok();
   if (!inl && !segs_dev) return fail(FLOWKV_EINVAL, "NULL segment list");
   if (!inl && reinterpret_cast<uintptr_t>(segs_dev) % 16)
@@ -525,7 +626,8 @@ int launch_transfer(const flowkv_pool* src, const flowkv_pool* dst,
   a.dst.num_blocks = dst->num_blocks;
   a.segs = inl ? nullptr : segs_dev;
   if (inl)
-    for (int64_t i = 0; i < n_segs; ++i) a.inline_runs[i] = segs_host[i];
+    if (!compact)
+      for (int64_t i = 0; i < n_segs; ++i) a.inline_runs[i] = segs_host[i];
   a.n_segs = int32_t(n_segs);
   a.num_layers = src->num_layers;
   a.chunk_bytes = src->chunk_bytes;
@@ -570,13 +672,29 @@ int launch_transfer(const flowkv_pool* src, const flowkv_pool* dst,
   }
   launch = std::min<int64_t>(launch, INT32_MAX);
 
-  KernelFn fn = pick_kernel(src->layout == FLOWKV_LAYOUT_LAYER_MAJOR,
-                            dst->layout == FLOWKV_LAYOUT_LAYER_MAJOR, unroll, cache - 1, uniform,
-                            inl);
-  void* args[] = {&a};
-  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(launch)),
-                                 dim3(unsigned(threads)), args, 0,
-                                 static_cast<hipStream_t>(hip_stream));
+  hipError_t e;
+  if (compact) {
+    XferArgsBM b{};
+    static_cast<XferShape&>(b) = static_cast<const XferShape&>(a);
+    b.src.base[0] = a.src.base[0];
+    b.src.num_blocks = a.src.num_blocks;
+    b.dst.base[0] = a.dst.base[0];
+    b.dst.num_blocks = a.dst.num_blocks;
+    for (int64_t i = 0; i < n_segs; ++i)
+      b.inline_runs[i] = CompactRun{segs_host[i].src_block, segs_host[i].dst_block,
+                                    segs_host[i].first};
+    KernelFnBM fn = pick_kernel_bm(unroll, cache - 1, uniform);
+    void* args[] = {&b};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(launch)),
+                        dim3(unsigned(threads)), args, 0, static_cast<hipStream_t>(hip_stream));
+  } else {
+    KernelFn fn = pick_kernel(src->layout == FLOWKV_LAYOUT_LAYER_MAJOR,
+                              dst->layout == FLOWKV_LAYOUT_LAYER_MAJOR, unroll, cache - 1,
+                              uniform, inl);
+    void* args[] = {&a};
+    e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(launch)),
+                        dim3(unsigned(threads)), args, 0, static_cast<hipStream_t>(hip_stream));
+  }
   if (e == hipSuccess) e = hipGetLastError();
   if (e != hipSuccess) return fail(FLOWKV_EHIP, "kernel launch: %s", hipGetErrorString(e));
   return ok();

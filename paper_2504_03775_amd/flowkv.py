@@ -25,6 +25,7 @@ POLICY_SEGMENT, POLICY_FIFO_SORTED, POLICY_FIFO_SHUFFLED = 0, 1, 2
 LAYOUT_LAYER_MAJOR, LAYOUT_BLOCK_MAJOR = 0, 1
 MAX_LAYERS = 128
 INLINE_RUNS = 64  # plan records flowkv_transfer_inline carries in the kernel arguments
+INLINE_RUNS_BLOCK_MAJOR = 300  # ... between two block-major pools, in the planner's form
 
 SEGMENT_DTYPE = np.dtype([("src_block", "<i4"), ("dst_block", "<i4"),
                           ("n_blocks", "<i4"), ("first", "<i4")])
@@ -434,11 +435,20 @@ def flowkv_transfer_ex(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_bl
            "flowkv_transfer_ex")
 
 
+def inline_capacity(src: KVPool, dst: KVPool) -> int:
+    """Most plan records (as flowkv_plan writes them) that flowkv_transfer_inline
+    carries in the kernel arguments between these two pools."""
+    both_bm = src.layout == LAYOUT_BLOCK_MAJOR and dst.layout == LAYOUT_BLOCK_MAJOR
+    return INLINE_RUNS_BLOCK_MAJOR if both_bm else INLINE_RUNS
+
+
 def flowkv_transfer_inline(src: KVPool, dst: KVPool, segs: np.ndarray, total_blocks: int,
                            threads: int = 0, unroll: int = 0, grid: int = 0, cache: int = 0,
                            order: int = 0, stream=None) -> None:
-    """Enqueue the one-launch copy with a host plan (SEGMENT_DTYPE array of at
-    most INLINE_RUNS records) carried in the kernel arguments."""
+    """Enqueue the one-launch copy with a host plan (SEGMENT_DTYPE array)
+    carried in the kernel arguments: at most INLINE_RUNS records, or
+    INLINE_RUNS_BLOCK_MAJOR in the planner's form between block-major pools
+    (``inline_capacity``)."""
     segs = np.ascontiguousarray(segs, dtype=SEGMENT_DTYPE)
     cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
     _check(_lib.flowkv_transfer_inline(ctypes.byref(src.desc), ctypes.byref(dst.desc),

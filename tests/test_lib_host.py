@@ -41,6 +41,7 @@ def test_binding_constants_match_the_header():
     text = open(os.path.join(ROOT, "include", "flowkv.h")).read()
     defines = dict(re.findall(r"#define\s+(FLOWKV_\w+)\s+(-?\d+)", text))
     assert int(defines["FLOWKV_INLINE_RUNS"]) == fk.INLINE_RUNS
+    assert int(defines["FLOWKV_INLINE_RUNS_BLOCK_MAJOR"]) == fk.INLINE_RUNS_BLOCK_MAJOR
     enums = dict(re.findall(r"\b(FLOWKV_E?\w+)\s*=\s*(-?\d+)", text))
     for name in ("OK", "EINVAL", "ENOSPC", "ERANGE", "EDUP", "ECAP", "EHIP", "ENOMEM"):
         assert int(enums["FLOWKV_" + name]) == getattr(fk, name), name
@@ -334,6 +335,30 @@ def test_transfer_rejects_bad_pools_without_touching_the_device():
     rc = fk.lib().flowkv_transfer_inline(ctypes.byref(good_src), ctypes.byref(good_dst),
                                          big.ctypes.data_as(fk._SEGP), len(big), 1, None, None)
     assert rc == fk.ECAP
+    # beyond INLINE_RUNS only between block-major pools, only in the
+    # planner's form, and at most INLINE_RUNS_BLOCK_MAJOR records
+    def inline(src, dst, recs, total):
+        return fk.lib().flowkv_transfer_inline(ctypes.byref(src), ctypes.byref(dst),
+                                               recs.ctypes.data_as(fk._SEGP), len(recs), total,
+                                               None, None)
+
+    def planner_form(k):
+        r = np.zeros(k, dtype=fk.SEGMENT_DTYPE)
+        r["n_blocks"], r["first"] = 1, np.arange(k)
+        return r
+    assert inline(good_src, good_dst, planner_form(fk.INLINE_RUNS_BLOCK_MAJOR + 1),
+                  fk.INLINE_RUNS_BLOCK_MAJOR + 1) == fk.ECAP
+    runs = planner_form(100)
+    lm_src = pool(layout=0, L=2, bases=(1 << 34, (1 << 34) + (1 << 24)))
+    assert inline(lm_src, good_dst, runs, 100) == fk.ECAP        # layer-major sender
+    gap = runs.copy()
+    gap["first"][50] += 1
+    assert inline(good_src, good_dst, gap, 100) == fk.ECAP       # runs do not abut
+    assert inline(good_src, good_dst, runs, 101) == fk.ECAP      # nor cover total_blocks
+    empty = runs.copy()
+    empty["n_blocks"][7] = 0
+    empty["first"][8:] -= 1
+    assert inline(good_src, good_dst, empty, 99) == fk.ECAP      # a run of no blocks
     rc = fk.lib().flowkv_transfer_inline(ctypes.byref(good_src), ctypes.byref(good_dst),
                                          None, 1, 1, None, None)
     assert rc == fk.EINVAL

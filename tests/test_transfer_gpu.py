@@ -285,14 +285,16 @@ def test_llama8b_13k_full_size(policy, sl, dl):
     say(f"  {len(segs)} runs, {nb} blocks checked, {nk} untouched checked")
 
 
-@pytest.mark.parametrize("sl,dl", [(BM, BM), (LM, BM)], ids=lambda x: NAMES[x])
-def test_llama8b_13k_full_size_plan_in_kernel_arguments(sl, dl):
-    """The 13k request with the segment-allocator receiver (43 runs) in the
-    launch bench.py times for it: the plan carried in the kernel's
-    arguments."""
-    wl, ref = build(recipes.llama8b_13k, "segment")
+@pytest.mark.parametrize("policy,sl,dl", [("segment", BM, BM), ("segment", LM, BM),
+                                          ("fifo_sorted", BM, BM)])
+def test_llama8b_13k_full_size_plan_in_kernel_arguments(policy, sl, dl):
+    """The 13k request in the launch bench.py times for it: the plan carried
+    in the kernel's arguments -- 43 runs from the segment-allocator receiver,
+    255 (12-byte records, block-major pools) from the free-list receiver."""
+    wl, ref = build(recipes.llama8b_13k, policy)
     segs, nb, nk = check_sampled(wl, ref, sl, dl, inline=True)
-    assert len(segs) <= fk.INLINE_RUNS and nb == 813
+    assert nb == 813
+    assert len(segs) <= (fk.INLINE_RUNS_BLOCK_MAJOR if (sl, dl) == (BM, BM) else fk.INLINE_RUNS)
     say(f"  inline: {len(segs)} runs, {nb} blocks checked, {nk} untouched checked")
 
 
@@ -388,6 +390,44 @@ def test_inline_plans_against_oracle(seed):
     assert host_equal(download_all(dst), h_dst)
 
 
+@pytest.mark.parametrize("seed", range(10))
+def test_compact_inline_plans_against_oracle(seed):
+    """Plans of 65 to 300 runs between block-major pools, carried in the
+    kernel arguments as 12-byte records: random geometries (both the uniform
+    and the per-lane path), runs of 1 to 3 blocks, random launch shapes."""
+    g = np.random.default_rng(5000 + seed)
+    geoms = [Geometry("c1", 2, 2, 64, 16, "float16"), Geometry("c2", 3, 3, 40, 16, "bfloat16"),
+             Geometry("c3", 1, 1, 128, 5, "float16")]
+    geom = geoms[seed % len(geoms)]
+    k = int(g.integers(fk.INLINE_RUNS + 1, fk.INLINE_RUNS_BLOCK_MAJOR + 1))
+    if seed == 0:
+        k = fk.INLINE_RUNS_BLOCK_MAJOR
+    lens = g.integers(1, 4, size=k)
+    n = int(lens.sum())
+    B = 2 * n + 8
+    # runs that cannot merge: each run's sender start jumps ahead
+    S, D, s0, d0 = [], [], 0, int(g.integers(0, 4))
+    for m in lens:
+        S.extend(range(s0, s0 + m))
+        D.extend(range(d0, d0 + m))
+        s0 += m + 1
+        d0 += m + int(g.integers(0, 2))
+    S, D = np.array(S, np.int32), np.array(D, np.int32)
+    assert S.max() < B and D.max() < B
+    segs = fk.flowkv_plan(S, D, B, B)
+    assert len(segs) == k
+    cfg = CONFIGS[seed % len(CONFIGS)]
+    say(f"compact inline seed={seed} runs={k} blocks={n} geom={geom.name} cfg={cfg}")
+    src = device_pool(geom, BM, B, seed)
+    dst = device_pool(geom, BM, B, seed + 1)
+    h_src, h_dst = download_all(src), download_all(dst)
+    fk.flowkv_transfer_inline(src, dst, segs, n, **cfg)
+    torch.cuda.synchronize()
+    oracle.transfer_fast(h_src, h_dst, S, D)
+    got = download_all(dst)
+    assert host_equal(got, h_dst), first_mismatch(got, h_dst)
+
+
 def test_inline_plan_at_the_limit_equals_device_plan():
     """64 one-block runs (the inline limit) at the 8B geometry: the inline and
     the device-memory plan give the same receiver pool, and match the oracle."""
@@ -402,6 +442,30 @@ def test_inline_plan_at_the_limit_equals_device_plan():
     assert len(segs) == fk.INLINE_RUNS
     fk.flowkv_transfer_inline(src, d1, segs, 64)
     fk.flowkv_transfer(src, d2, fk.segments_to_device(segs, src.device), len(segs), 64)
+    torch.cuda.synchronize()
+    oracle.transfer_fast(h_src, h_dst, S, D)
+    got = download_all(d1)
+    assert host_equal(got, h_dst)
+    assert host_equal(got, download_all(d2))
+
+
+def test_compact_inline_plan_at_the_limit_equals_device_plan():
+    """300 one-block runs (the block-major inline limit) at the 8B geometry:
+    the compact inline plan and the device-memory plan give the same receiver
+    pool, and match the oracle."""
+    geom = LLAMA3_8B
+    k = fk.INLINE_RUNS_BLOCK_MAJOR
+    B = 2 * k + 2
+    src = device_pool(geom, BM, B, 0)
+    d1 = device_pool(geom, BM, B, 1)
+    d2 = device_pool(geom, BM, B, 1)
+    h_src, h_dst = download_all(src), download_all(d1)
+    S = 2 * np.arange(k, dtype=np.int32)
+    D = 2 * np.arange(k, dtype=np.int32) + 1
+    segs = fk.flowkv_plan(S, D, B, B)
+    assert len(segs) == k
+    fk.flowkv_transfer_inline(src, d1, segs, k)
+    fk.flowkv_transfer(src, d2, fk.segments_to_device(segs, src.device), len(segs), k)
     torch.cuda.synchronize()
     oracle.transfer_fast(h_src, h_dst, S, D)
     got = download_all(d1)
