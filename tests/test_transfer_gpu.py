@@ -207,7 +207,8 @@ def test_plan_stager_on_idle_and_busy_streams():
         if i % 3 == 0:
             torch.cuda.synchronize()          # idle: the copy goes on the stream
         else:
-            filler.fill_(i)                   # busy: the copy goes on the side stream
+            for _ in range(8):                # busy (about 0.3 ms of queued fills): the
+                filler.fill_(i)               # copy goes on the side stream
         seen.add(stream.query())
         dev = stager.stage(segs, stream)
         fk.flowkv_transfer_ex(src, dst, dev, len(segs), n, stream=stream)
