@@ -147,7 +147,9 @@ typedef struct flowkv_launch_config {
 
 /* Create an allocator over block IDs [0, num_blocks), all free.  `seed` is used
    by FLOWKV_POLICY_FIFO_SHUFFLED only.  *out receives the handle.
-   EINVAL: num_blocks < 0, unknown policy, out == NULL. */
+   EINVAL: num_blocks < 0, unknown policy, out == NULL.  ENOMEM: host memory
+   ran out (nothing is created).  The other allocator and planner calls also
+   return ENOMEM if host memory runs out mid-call (see the status codes). */
 int flowkv_allocator_create(int32_t num_blocks, int32_t policy, uint64_t seed,
                             flowkv_allocator** out);
 
