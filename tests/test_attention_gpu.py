@@ -181,13 +181,16 @@ def test_length_caps_and_empty_request():
     assert np.all(z == 0)
 
 
+@pytest.mark.parametrize("hq", [8, 16], ids=["vector-pass", "matrix-core-pass"])
 @pytest.mark.parametrize("layout", [BM, LM], ids=lambda x: NAMES[x])
-def test_blocks_outside_the_pool_contribute_nothing(layout):
+def test_blocks_outside_the_pool_contribute_nothing(layout, hq):
     """A block ID outside the pool (negative or >= the pool's size) inside a
     request's length is skipped: the output equals attention over the tokens
-    of the valid blocks alone (attention does not depend on token order)."""
+    of the valid blocks alone (attention does not depend on token order).
+    8 query heads on 2 KV heads run the vector pass, 16 the matrix-core pass
+    (where a hole falls inside a 32-token tile, split 64: two tiles)."""
     geom = Geometry("holes", 3, 2, 128, 16, "bfloat16")
-    B, layer, hq, bs = 50, 1, 8, 16
+    B, layer, bs = 50, 1, 16
     pool = fk.KVPool(layout, make_device_pool(geom, layout, B, "cuda", 21))
     g = np.random.default_rng(21)
     perm = g.permutation(B).astype(np.int32)
@@ -226,6 +229,22 @@ def test_blocks_outside_the_pool_contribute_nothing(layout):
     err = np.abs(got - want).max()
     assert np.all(np.isfinite(got))
     assert err <= 2e-4 * vmax + 1e-6, err
+
+
+@pytest.mark.parametrize("layout", [BM, LM], ids=lambda x: NAMES[x])
+@pytest.mark.parametrize("split", [32, 64, 128, 160, 256, 384, 1024])
+def test_matrix_core_pass_tile_counts(layout, split):
+    """The matrix-core pass (8 query heads per KV head, head_dim 128) takes
+    32-token tiles, 4 waves a workgroup, and issues each tile's loads one tile
+    ahead into alternating buffers.  Lengths around tile and step edges
+    (1, 31..33, 127..129, 255, 257, 1000) under these split lengths give waves
+    0 to 8 tiles, odd and even counts, full and ragged last tiles."""
+    geom = Geometry("tiles", 2, 2, 128, 16, "bfloat16")
+    lens = [1, 31, 32, 33, 127, 128, 129, 255, 257, 1000]
+    blocks = sum(-(-T // 16) for T in lens) + 8
+    say(f"matrix-core tiles {NAMES[layout]} split={split}")
+    _, err = run_case(geom, layout, blocks, lens, 16, 40 + split, split, layer=1)
+    say(f"  max error {err:.2e}")
 
 
 # ---- the bench's attention workloads at full size ------------------------------
