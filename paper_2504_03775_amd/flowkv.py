@@ -176,11 +176,38 @@ def _i32(a) -> np.ndarray:
     return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
 
 
-def _ptr(a: np.ndarray, t=None) -> int:
+def _ptr(a: np.ndarray) -> int:
     """The array's address, for a c_void_p argument (a typed ctypes pointer
     costs several microseconds per call to build, and the array interface
     dictionary of a structured array as much)."""
     return a.ctypes.data
+
+
+def _host_segments(segs) -> np.ndarray:
+    """A host plan as a contiguous SEGMENT_DTYPE array: one already, or an
+    integer (k, 4) array of (src_block, dst_block, n_blocks, first) rows."""
+    a = np.asarray(segs)
+    if a.dtype == SEGMENT_DTYPE:
+        return np.ascontiguousarray(a).reshape(-1)
+    if a.dtype.kind in "iu" and a.ndim == 2 and a.shape[1] == 4:
+        return np.ascontiguousarray(a, dtype=np.int32).view(SEGMENT_DTYPE).reshape(-1)
+    raise ValueError(f"a plan is a SEGMENT_DTYPE array or an integer (k, 4) array, "
+                     f"not {a.dtype} {a.shape}")
+
+
+def _device_segments(segs_dev, n_segs: int, pool: "KVPool") -> int:
+    """Address of a device plan: a contiguous int32 tensor of at least n_segs
+    rows of 4 on the pools' device (0 when n_segs is 0)."""
+    if n_segs <= 0:
+        return 0
+    import torch
+
+    if segs_dev.dtype != torch.int32 or not segs_dev.is_contiguous() \
+            or segs_dev.device != pool.device or segs_dev.numel() < 4 * n_segs:
+        raise ValueError(f"device plan: need a contiguous int32 tensor of >= {n_segs} x 4 "
+                         f"on {pool.device}, got {segs_dev.dtype} {tuple(segs_dev.shape)} "
+                         f"on {segs_dev.device}")
+    return segs_dev.data_ptr()
 
 
 # ---- allocator ---------------------------------------------------------------
@@ -318,10 +345,10 @@ class Scheduler:
                 or spb.shape != (n, n) or lat.shape != (n, n):
             raise ValueError("routing arrays do not match the node count")
         pn, dn = ctypes.c_int32(), ctypes.c_int32()
-        _check(_lib.flowkv_sched_route(self._h, prompt_tokens, _ptr(hit, _I64P), _ptr(q, _I64P),
+        _check(_lib.flowkv_sched_route(self._h, prompt_tokens, _ptr(hit), _ptr(q),
                                        _ptr(rate), kv_bytes,
                                        _ptr(spb), _ptr(lat),
-                                       _ptr(free, _I64P), ctypes.byref(pn), ctypes.byref(dn)),
+                                       _ptr(free), ctypes.byref(pn), ctypes.byref(dn)),
                "flowkv_sched_route")
         return pn.value, dn.value
 
@@ -349,7 +376,7 @@ def flowkv_plan_batch(offsets, src_ids, dst_ids, src_pool_blocks: int,
         raise ValueError("sender and receiver lists differ in length")
     out = np.empty(max(s.size, 1), dtype=SEGMENT_DTYPE)
     n = ctypes.c_int64()
-    _check(_lib.flowkv_plan_batch(off.size - 1, _ptr(off, _I64P), _ptr(s), _ptr(d),
+    _check(_lib.flowkv_plan_batch(off.size - 1, _ptr(off), _ptr(s), _ptr(d),
                                   src_pool_blocks, dst_pool_blocks, _ptr(out),
                                   out.size, ctypes.byref(n)), "flowkv_plan_batch")
     return out[: n.value]
@@ -417,10 +444,11 @@ def _stream_handle(stream) -> Optional[int]:
 
 def flowkv_transfer(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_blocks: int,
                     stream=None) -> None:
-    """Enqueue the one-launch copy; segs_dev is a device int32 (k, 4) tensor."""
+    """Enqueue the one-launch copy; segs_dev is a device int32 (k, 4) tensor
+    on the pools' device."""
     _check(_lib.flowkv_transfer(ctypes.byref(src.desc), ctypes.byref(dst.desc),
-                                ctypes.c_void_p(segs_dev.data_ptr() if n_segs else 0), n_segs,
-                                total_blocks, ctypes.c_void_p(_stream_handle(stream))),
+                                ctypes.c_void_p(_device_segments(segs_dev, n_segs, src)),
+                                n_segs, total_blocks, ctypes.c_void_p(_stream_handle(stream))),
            "flowkv_transfer")
 
 
@@ -429,7 +457,7 @@ def flowkv_transfer_ex(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_bl
                        order: int = 0, stream=None) -> None:
     cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
     _check(_lib.flowkv_transfer_ex(ctypes.byref(src.desc), ctypes.byref(dst.desc),
-                                   ctypes.c_void_p(segs_dev.data_ptr() if n_segs else 0),
+                                   ctypes.c_void_p(_device_segments(segs_dev, n_segs, src)),
                                    n_segs, total_blocks, ctypes.byref(cfg),
                                    ctypes.c_void_p(_stream_handle(stream))),
            "flowkv_transfer_ex")
@@ -445,11 +473,11 @@ def inline_capacity(src: KVPool, dst: KVPool) -> int:
 def flowkv_transfer_inline(src: KVPool, dst: KVPool, segs: np.ndarray, total_blocks: int,
                            threads: int = 0, unroll: int = 0, grid: int = 0, cache: int = 0,
                            order: int = 0, stream=None) -> None:
-    """Enqueue the one-launch copy with a host plan (SEGMENT_DTYPE array)
-    carried in the kernel arguments: at most INLINE_RUNS records, or
-    INLINE_RUNS_BLOCK_MAJOR in the planner's form between block-major pools
-    (``inline_capacity``)."""
-    segs = np.ascontiguousarray(segs, dtype=SEGMENT_DTYPE)
+    """Enqueue the one-launch copy with a host plan (SEGMENT_DTYPE array, or
+    int (k, 4) rows) carried in the kernel arguments: at most INLINE_RUNS
+    records, or INLINE_RUNS_BLOCK_MAJOR in the planner's form between
+    block-major pools (``inline_capacity``)."""
+    segs = _host_segments(segs)
     cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
     _check(_lib.flowkv_transfer_inline(ctypes.byref(src.desc), ctypes.byref(dst.desc),
                                        _ptr(segs), len(segs), total_blocks,
@@ -463,7 +491,7 @@ def flowkv_transfer_layers(src: KVPool, dst: KVPool, segs_dev, n_segs: int, tota
     """Enqueue the copy of layers [layer_begin, layer_begin + layer_count) only."""
     cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
     _check(_lib.flowkv_transfer_layers(ctypes.byref(src.desc), ctypes.byref(dst.desc),
-                                       ctypes.c_void_p(segs_dev.data_ptr() if n_segs else 0),
+                                       ctypes.c_void_p(_device_segments(segs_dev, n_segs, src)),
                                        n_segs, total_blocks, layer_begin, layer_count,
                                        ctypes.byref(cfg), ctypes.c_void_p(_stream_handle(stream))),
            "flowkv_transfer_layers")
@@ -519,7 +547,7 @@ def segments_to_device(segs: np.ndarray, device, stream=None):
     that reads it (torch's caching allocator keeps it while referenced)."""
     import torch
 
-    host = torch.from_numpy(np.ascontiguousarray(segs).view(np.int32).reshape(-1, 4))
+    host = torch.from_numpy(_host_segments(segs).view(np.int32).reshape(-1, 4))
     pinned = host.pin_memory()
     if stream is None:
         return pinned.to(device, non_blocking=True)
@@ -575,7 +603,7 @@ class PlanStager:
         if self.used[j]:
             self.done[j].synchronize()
         if k:
-            self.host[j].numpy()[:k] = np.ascontiguousarray(segs).view(np.int32).reshape(-1, 4)
+            self.host[j].numpy()[:k] = _host_segments(segs).view(np.int32).reshape(-1, 4)
             if stream.query():
                 with torch.cuda.stream(stream):
                     self.dev[j][:k].copy_(self.host[j][:k], non_blocking=True)

@@ -278,6 +278,37 @@ def test_plan_errors():
     assert len(fk.flowkv_plan([], [], P, P)) == 0
 
 
+def test_binding_marshals_plans_or_rejects_them():
+    """A host plan is taken as SEGMENT_DTYPE records or as integer (k, 4)
+    rows of the same four fields (any integer width), anything else is
+    rejected; a device plan must be a contiguous int32 tensor of at least
+    n_segs rows on the pools' device (no device is touched here)."""
+    import torch
+    from types import SimpleNamespace
+
+    plan = fk.flowkv_plan([3, 4, 9], [7, 8, 1], 16, 16)
+    rows = plan.view(np.int32).reshape(-1, 4)
+    for form in (plan, rows, rows.astype(np.int64), rows.astype(np.uint16), rows.tolist()):
+        got = fk._host_segments(form)
+        assert got.dtype == fk.SEGMENT_DTYPE and got.flags.c_contiguous
+        assert np.array_equal(got.view(np.int32).reshape(-1, 4), rows)
+    assert len(fk._host_segments(np.zeros((0, 4), np.int32))) == 0
+    for bad in (rows.astype(np.float32), rows[:, :3], rows.reshape(-1), rows.reshape(1, -1, 4)):
+        with pytest.raises(ValueError):
+            fk._host_segments(bad)
+
+    on = SimpleNamespace(device=torch.device("cuda", 0))
+    t = torch.from_numpy(rows.copy())                 # a CPU tensor: wrong device
+    assert fk._device_segments(t, 0, on) == 0         # nothing to read, nothing checked
+    with pytest.raises(ValueError, match="device plan"):
+        fk._device_segments(t, 2, on)
+    cpu = SimpleNamespace(device=torch.device("cpu"))
+    assert fk._device_segments(t, 2, cpu) == t.data_ptr()
+    for bad in (t.to(torch.int64), t.t(), t[:1]):     # dtype, layout, too few rows
+        with pytest.raises(ValueError, match="device plan"):
+            fk._device_segments(bad, 2, cpu)
+
+
 # ---- transfer argument checks (rejected before any device call) --------------
 
 def pool(layout=1, L=2, B=8, chunk=4096, bases=(1 << 20,)):
