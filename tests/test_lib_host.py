@@ -249,6 +249,76 @@ def test_planners_are_reentrant_across_threads():
     assert not errors, errors
 
 
+def first_repeat(ids):
+    """Position of the first ID that appeared at an earlier position, or None."""
+    seen = set()
+    for i, x in enumerate(ids):
+        if x in seen:
+            return i
+        seen.add(x)
+    return None
+
+
+def raw_plan(S, D, P, cap, fill=-9):
+    """flowkv_plan with an explicit capacity; returns (code, n_out, records)."""
+    S, D = np.ascontiguousarray(S, np.int32), np.ascontiguousarray(D, np.int32)
+    out = np.full(4 * max(cap, 1), fill, dtype=np.int32).view(fk.SEGMENT_DTYPE)
+    n = ctypes.c_int64(-1)
+    rc = fk.lib().flowkv_plan(S.ctypes.data, D.ctypes.data, len(S), P, P, out.ctypes.data, cap,
+                              ctypes.byref(n))
+    return rc, n.value, out
+
+
+def test_plan_repeats_capacities_and_reuse_after_errors():
+    """Repeats are found a run of IDs at a time: the reported position is the
+    first whose ID appeared earlier (receiver list first, then sender);
+    an output with room for one record per block is written in the counting
+    pass, a smaller one after counting, and ECAP leaves it untouched; after
+    every rejected plan the same IDs plan cleanly on the same thread."""
+    g = np.random.default_rng(23)
+    P = 300
+    for case in range(400):
+        n = int(g.integers(2, 60))
+        # runs of consecutive IDs, as allocators hand them out
+        def table():
+            ids, x = [], int(g.integers(0, P))
+            while len(ids) < n:
+                if g.random() < 0.3:
+                    x = int(g.integers(0, P))
+                ids.append(x % P)
+                x += 1
+            return ids
+        S, D = table(), table()
+        rs, rd = first_repeat(S), first_repeat(D)
+        rc, _, _ = raw_plan(S, D, P, n)
+        if rd is not None or rs is not None:
+            assert rc == fk.EDUP, (case, S, D)
+            pos, bad = (rd, D) if rd is not None else (rs, S)
+            msg = fk.lib().flowkv_last_error().decode()
+            assert f"block {bad[pos]} repeated (position {pos})" in msg, (msg, pos, S, D)
+            assert msg.startswith("receiver" if rd is not None else "sender"), msg
+            # the bits set before the repeat were cleared: the distinct IDs
+            # of both lists, in order, plan cleanly now
+            S, D = list(dict.fromkeys(S)), list(dict.fromkeys(D))
+            k = min(len(S), len(D))
+            S, D = S[:k], D[:k]
+        want = oracle.plan_ref(S, D)
+        need, total = len(want), len(S)
+        for cap in sorted({need, total, total + 3}):
+            rc, k, out = raw_plan(S, D, P, cap)
+            assert rc == fk.OK and k == need, (case, cap, rc)
+            assert as_tuples(out[:k]) == want
+            assert (out["first"][:k] == np.concatenate(([0], np.cumsum(out["n_blocks"][:k])[:-1]))).all()
+        if need > 1:
+            rc, k, out = raw_plan(S, D, P, need - 1)
+            assert rc == fk.ECAP and k == need
+            assert (out.view(np.int32) == -9).all(), "ECAP wrote into the output"
+    # a range error after a valid plan of the same IDs leaves nothing behind
+    with pytest.raises(fk.FlowKVError):
+        fk.flowkv_plan([0, 1, 2], [5, 6, P], P, P)
+    assert as_tuples(fk.flowkv_plan([0, 1, 2], [5, 6, 7], P, P)) == [(0, 5, 3)]
+
+
 def test_plan_errors():
     P = 16
     cases = [((P,), (0,), fk.ERANGE), ((0,), (-1,), fk.ERANGE), ((1, 1), (2, 3), fk.EDUP),
