@@ -299,11 +299,13 @@ def test_llama8b_13k_full_size_plan_in_kernel_arguments(policy, sl, dl):
     say(f"  inline: {len(segs)} runs, {nb} blocks checked, {nk} untouched checked")
 
 
-@pytest.mark.parametrize("policy", ["segment", "fifo_shuffled"])
-def test_batch32_full_size(policy):
+@pytest.mark.parametrize("policy,sl,dl", [("segment", BM, BM), ("fifo_shuffled", BM, BM),
+                                          ("segment", LM, LM)])
+def test_batch32_full_size(policy, sl, dl):
     wl, ref = build(recipes.batch32, policy)
-    say(f"batch32 {policy}: {wl.n_blocks} blocks, pools {wl.src_pool_blocks}/{wl.dst_pool_blocks}")
-    segs, nb, nk = check_sampled(wl, ref, BM, BM)
+    say(f"batch32 {policy} {NAMES[sl]}->{NAMES[dl]}: {wl.n_blocks} blocks, "
+        f"pools {wl.src_pool_blocks}/{wl.dst_pool_blocks}")
+    segs, nb, nk = check_sampled(wl, ref, sl, dl)
     if policy == "segment":
         assert len(segs) == 32
     say(f"  {len(segs)} runs, {nb} blocks checked")
@@ -319,11 +321,12 @@ def test_llama70b_tp8_full_size(policy, sl, dl):
     say(f"  {len(segs)} runs, {nb} blocks checked")
 
 
-@pytest.mark.parametrize("variant", ["segment", "shuffled", "stride2"])
-def test_churn_full_size(variant):
+@pytest.mark.parametrize("variant,sl,dl", [("segment", BM, BM), ("shuffled", BM, BM),
+                                           ("stride2", BM, BM), ("shuffled", LM, BM)])
+def test_churn_full_size(variant, sl, dl):
     wl, ref = build(recipes.churn, variant)
-    say(f"churn {variant}: {wl.n_blocks} blocks")
-    segs, nb, nk = check_sampled(wl, ref, BM, BM)
+    say(f"churn {variant} {NAMES[sl]}->{NAMES[dl]}: {wl.n_blocks} blocks")
+    segs, nb, nk = check_sampled(wl, ref, sl, dl)
     if variant == "stride2":
         assert len(segs) == wl.n_blocks
     say(f"  {len(segs)} runs, {nb} blocks checked")
