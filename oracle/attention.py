@@ -19,9 +19,10 @@ of ``oracle.kvcopy.slot_address`` (both Eq. 5 layouts).
 
 Parity: pinned in ``tests/test_oracle_attention.py`` -- one token returns its
 V exactly, equal scores average V, a query that singles out one key returns
-that key's V, agreement with a separate dense softmax-attention computed from
-numpy's einsum on a contiguous copy, and invariance under relabelling the
-pool's blocks.
+that key's V, with a constant V per KV head every query head returns its
+group's constant, agreement with a separate dense softmax-attention computed
+from numpy's einsum on a contiguous copy, and invariance under relabelling
+the pool's blocks.
 """
 
 from __future__ import annotations

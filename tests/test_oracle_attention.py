@@ -117,6 +117,25 @@ def test_closed_forms(layout):
     np.testing.assert_allclose(got[0, 0], from_bf16(kv[1, j, 0]), rtol=1e-12, atol=1e-30)
 
 
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_query_heads_read_their_group_kv_head(layout):
+    """Grouped KV heads: query head h reads KV head h // (Hq / Hkv).  With
+    every token's V of KV head g equal to the constant g + 1, query head h's
+    output is (h // G) + 1 whatever q and K are: the weights sum to one."""
+    rng = np.random.default_rng(4)
+    L, B, bs, hkv, dh, hq = 2, 8, 4, 4, 8, 8       # G = 2
+    T = 11
+    k = rng.standard_normal((T, hkv, dh))
+    v = np.broadcast_to((np.arange(hkv) + 1.0)[None, :, None], (T, hkv, dh))
+    kv = np.stack([to_bf16(k), to_bf16(v)])
+    table = [5, 2, 7]
+    pool = build_pool(layout, L, B, bs, hkv, dh, 1, [table], [kv])
+    q = rng.standard_normal((1, hq, dh)) * 3.0
+    got = decode_attention(pool, q, [table], [T], 1, hkv, dh, 0.7)
+    want = (np.arange(hq) // (hq // hkv) + 1.0)[:, None] * np.ones(dh)
+    np.testing.assert_allclose(got[0], want, rtol=1e-13, atol=0)
+
+
 def test_block_relabelling_does_not_change_the_result():
     rng = np.random.default_rng(3)
     L, B, bs, hkv, dh, hq = 2, 10, 4, 2, 8, 4
