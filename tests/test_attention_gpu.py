@@ -250,14 +250,18 @@ def test_matrix_core_pass_tile_counts(layout, split):
 # ---- the bench's attention workloads at full size ------------------------------
 
 def download_layer(pool: fk.KVPool, ids, layer: int) -> oracle.HostPool:
-    """K and V of one layer of blocks `ids` of a block-major device pool, as a
-    compact one-layer block-major host pool (block i = block ids[i])."""
+    """K and V of one layer of blocks `ids` of a device pool (either layout),
+    as a compact one-layer block-major host pool (block i = block ids[i])."""
     idx = torch.as_tensor(np.asarray(ids, dtype=np.int64), device=pool.device)
     slot = pool.kv_heads * pool.head_dim * pool.elem_bytes
     hp = oracle.HostPool.zeros(BM, 1, len(ids), pool.block_size, slot)
     out = hp.buffers[0].reshape(len(ids), -1)
     for lo in range(0, len(ids), 4096):
-        sub = pool.tensors[0].index_select(0, idx[lo:lo + 4096])[:, layer].contiguous()
+        if pool.layout == BM:   # (B, L, 2, bs, Hkv, Dh) -> (k, 2, bs, Hkv, Dh)
+            sub = pool.tensors[0].index_select(0, idx[lo:lo + 4096])[:, layer].contiguous()
+        else:                   # layer tensor (2, B, bs, Hkv, Dh) -> (k, 2, bs, Hkv, Dh)
+            sub = pool.tensors[layer].index_select(1, idx[lo:lo + 4096]).transpose(0, 1)
+            sub = sub.contiguous()
         out[lo:lo + 4096] = sub.view(torch.uint8).reshape(sub.shape[0], -1).cpu().numpy()
     return hp
 
@@ -269,19 +273,21 @@ BENCH_ATTN = {  # as bench.py --op attention builds them: recipe, query heads
 }
 
 
-@pytest.mark.parametrize("name", sorted(BENCH_ATTN))
-def test_bench_attention_workloads_full_size(name):
+@pytest.mark.parametrize("name,layout", [(w, BM) for w in sorted(BENCH_ATTN)] + [("batch", LM)],
+                         ids=lambda x: NAMES.get(x, x) if isinstance(x, int) else x)
+def test_bench_attention_workloads_full_size(name, layout):
     """Each --op attention workload exactly as bench.py runs it: its recipe's
-    block lists, the full receiver pool (block-major, seeded N(0,1)), every
-    request in one call, the default split, the middle layer; the outputs of
-    a sample of requests (shortest, longest and two between) against the
-    oracle on just those requests' blocks of that layer."""
+    block lists, the full receiver pool (block-major, and for the batch also
+    layer-major as --layout layer runs it; seeded N(0,1)), every request in
+    one call, the default split, the middle layer; the outputs of a sample
+    of requests (shortest, longest and two between) against the oracle on
+    just those requests' blocks of that layer."""
     make, q_heads = BENCH_ATTN[name]
     wl = make(lambda P, pol, seed: fk.Allocator(P, pol, seed))
     geom = wl.geom
     gc.collect()
     torch.cuda.empty_cache()
-    pool = fk.KVPool(BM, make_device_pool(geom, BM, wl.dst_pool_blocks, "cuda", 1))
+    pool = fk.KVPool(layout, make_device_pool(geom, layout, wl.dst_pool_blocks, "cuda", 1))
     lens = np.asarray(wl.tokens, dtype=np.int32)
     n, max_seq = len(lens), int(lens.max())
     max_blocks = max(len(d) for _, d in wl.tables)
@@ -312,7 +318,7 @@ def test_bench_attention_workloads_full_size(name):
         pos += k
     want = decode_attention(host, bf16_to_f64(q[pick]), ctabs, [int(lens[r]) for r in pick], 0,
                             geom.kv_heads, geom.head_dim, scale)
-    vmax = float(pool.tensors[0][:, layer].abs().max())
+    vmax = float((pool.tensors[0][:, layer] if layout == BM else pool.tensors[layer]).abs().max())
     err = np.abs(got[pick] - want).max()
     tol = 2e-4 * vmax + 1e-6
     say(f"  max error {err:.2e} (tolerance {tol:.2e})")
