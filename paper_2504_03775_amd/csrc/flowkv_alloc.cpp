@@ -29,7 +29,7 @@ struct flowkv_allocator {
   int32_t num_blocks = 0;
   int32_t policy = FLOWKV_POLICY_SEGMENT;
   int64_t free_blocks = 0;
-  std::vector<uint8_t> used;  // 1 = in use
+  std::vector<uint8_t> used;  // 1 = in use (2: seen while a list is being checked)
 
   // FLOWKV_POLICY_SEGMENT
   std::map<int32_t, int32_t> by_start;            // start -> length
@@ -88,33 +88,45 @@ uint64_t splitmix64_next(uint64_t& state) {
   return z ^ (z >> 31);
 }
 
-// Check ids[0..n): all in range, pairwise distinct, and each in use (want_used)
-// or free (!want_used).  Returns the sorted copy through `sorted`.
-int check_ids(const flowkv_allocator* a, const int32_t* ids, int32_t n, bool want_used,
-              std::vector<int32_t>& sorted) {
+// Check ids[0..n): all in range (first, so ERANGE wins over EDUP), pairwise
+// distinct, and each in use (want_used) or free (!want_used).  The state
+// check marks each ID as seen in this list (used = 2) and undoes the marks
+// before returning, so nothing changes and no sorted copy is needed.
+int check_ids(flowkv_allocator* a, const int32_t* ids, int32_t n, bool want_used) {
   if (n < 0) return fail(FLOWKV_EINVAL, "negative block count %d", n);
   if (n > 0 && !ids) return fail(FLOWKV_EINVAL, "NULL block list");
   for (int32_t i = 0; i < n; ++i)
     if (ids[i] < 0 || ids[i] >= a->num_blocks)
       return fail(FLOWKV_ERANGE, "block %d outside [0, %d)", ids[i], a->num_blocks);
-  sorted.assign(ids, ids + n);
-  std::sort(sorted.begin(), sorted.end());
-  for (int32_t i = 1; i < n; ++i)
-    if (sorted[i] == sorted[i - 1]) return fail(FLOWKV_EDUP, "block %d listed twice", sorted[i]);
-  for (int32_t b : sorted)
-    if ((a->used[b] != 0) != want_used)
-      return fail(FLOWKV_EDUP, "block %d is %s", b, want_used ? "already free" : "already in use");
-  return FLOWKV_OK;
+  const uint8_t want = want_used ? 1 : 0;
+  int rc = FLOWKV_OK;
+  int32_t i = 0;
+  for (; i < n; ++i) {
+    uint8_t& u = a->used[ids[i]];
+    if (u == 2) {
+      rc = fail(FLOWKV_EDUP, "block %d listed twice", ids[i]);
+      break;
+    }
+    if (u != want) {
+      rc = fail(FLOWKV_EDUP, "block %d is %s", ids[i],
+                want_used ? "already free" : "already in use");
+      break;
+    }
+    u = 2;
+  }
+  for (int32_t j = 0; j < i; ++j) a->used[ids[j]] = want;
+  return rc;
 }
 
-// Call f(start, end) for each maximal ascending run of a sorted ID list.
+// Call f(start, end) for each maximal run of consecutive IDs (each one more
+// than the last) of ids[0..n), in list order.
 template <class F>
-void for_each_run(const std::vector<int32_t>& s, F f) {
-  size_t i = 0;
-  while (i < s.size()) {
-    size_t j = i + 1;
-    while (j < s.size() && s[j] == s[j - 1] + 1) ++j;
-    f(s[i], s[j - 1] + 1);
+void for_each_run(const int32_t* ids, int32_t n, F f) {
+  int32_t i = 0;
+  while (i < n) {
+    int32_t j = i + 1;
+    while (j < n && ids[j] == ids[j - 1] + 1) ++j;
+    f(ids[i], ids[j - 1] + 1);
     i = j;
   }
 }
@@ -200,29 +212,31 @@ int alloc_impl(flowkv_allocator* a, int32_t n, int32_t* out_ids) {
   return ok();
 }
 
+// Freed runs merge with free neighbours on both sides, so releasing them in
+// list order leaves the same maximal free runs as any other order.
 int free_impl(flowkv_allocator* a, const int32_t* ids, int32_t n) {
   if (!a) return fail(FLOWKV_EINVAL, "NULL allocator");
-  std::vector<int32_t> s;
-  int rc = check_ids(a, ids, n, /*want_used=*/true, s);
+  int rc = check_ids(a, ids, n, /*want_used=*/true);
   if (rc) return rc;
-  for (int32_t b : s) a->used[b] = 0;
+  for (int32_t i = 0; i < n; ++i) a->used[ids[i]] = 0;
   a->free_blocks += n;
   if (a->policy == FLOWKV_POLICY_SEGMENT)
-    for_each_run(s, [&](int32_t lo, int32_t hi) { a->release_run(lo, hi - lo); });
+    for_each_run(ids, n, [&](int32_t lo, int32_t hi) { a->release_run(lo, hi - lo); });
   else
     for (int32_t i = 0; i < n; ++i) a->fifo.push_back(ids[i]);
   return ok();
 }
 
+// A run of consecutive free IDs lies inside one maximal free run, also after
+// other runs of the same list were claimed.
 int mark_used_impl(flowkv_allocator* a, const int32_t* ids, int32_t n) {
   if (!a) return fail(FLOWKV_EINVAL, "NULL allocator");
-  std::vector<int32_t> s;
-  int rc = check_ids(a, ids, n, /*want_used=*/false, s);
+  int rc = check_ids(a, ids, n, /*want_used=*/false);
   if (rc) return rc;
-  for (int32_t b : s) a->used[b] = 1;
+  for (int32_t i = 0; i < n; ++i) a->used[ids[i]] = 1;
   a->free_blocks -= n;
   if (a->policy == FLOWKV_POLICY_SEGMENT) {
-    for_each_run(s, [&](int32_t lo, int32_t hi) { a->claim_range(lo, hi); });
+    for_each_run(ids, n, [&](int32_t lo, int32_t hi) { a->claim_range(lo, hi); });
   } else {
     std::deque<int32_t> kept;
     for (int32_t b : a->fifo)

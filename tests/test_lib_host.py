@@ -110,6 +110,56 @@ def test_allocator_matches_oracle_on_random_streams(policy, seed):
         assert a.stats() == r.stats()
 
 
+@pytest.mark.parametrize("policy", [fk.POLICY_SEGMENT, fk.POLICY_FIFO_SORTED,
+                                    fk.POLICY_FIFO_SHUFFLED])
+def test_allocator_any_order_and_rejected_lists(policy):
+    """Frees of any subset of held blocks in any order, marks of free blocks
+    in any order, and rejected lists (a repeat after valid IDs, a free block
+    among held ones, a held block among free ones) interleaved: the tables
+    and stats stay identical to the oracle's, and a rejected list changes
+    nothing."""
+    g = np.random.default_rng(31 + policy)
+    P = 257
+    a, r = both(P, policy, 9)
+    held = []
+    for _ in range(400):
+        op = g.random()
+        if op < 0.35:
+            n = int(g.integers(0, min(40, r.free_count()) + 1))
+            x, y = a.alloc(n), r.alloc(n)
+            assert x.tolist() == list(y)
+            held.extend(x.tolist())
+        elif op < 0.65 and held:
+            g.shuffle(held)
+            k = int(g.integers(1, len(held) + 1))
+            ids, held = held[:k], held[k:]
+            a.free(ids)
+            r.free(ids)
+        elif op < 0.8:
+            free_ids = np.setdiff1d(np.arange(P), np.asarray(held, dtype=np.int64))
+            ids = g.permutation(free_ids)[: int(g.integers(0, min(12, free_ids.size) + 1))]
+            a.mark_used(ids)
+            r.mark_used(ids)
+            held.extend(ids.tolist())
+        else:
+            before = a.stats()
+            free_ids = np.setdiff1d(np.arange(P), np.asarray(held, dtype=np.int64)).tolist()
+            bad = []
+            if held:
+                bad.append((a.free, held[:3] + [held[0]]))
+                if free_ids:
+                    bad.append((a.free, held[:2] + free_ids[:1]))
+                    bad.append((a.mark_used, free_ids[:2] + held[:1]))
+            if len(free_ids) > 1:
+                bad.append((a.mark_used, free_ids[:2] + [free_ids[1]]))
+            for fn, ids in bad:
+                with pytest.raises(fk.FlowKVError) as e:
+                    fn(ids)
+                assert e.value.code == fk.EDUP
+            assert a.stats() == before
+        assert a.stats() == r.stats()
+
+
 @pytest.mark.parametrize("variant", ["segment", "shuffled"])
 def test_churn_stream_full_size_identical_tables(variant):
     """The 10,000-op churn workload at its real pool size (65,536 blocks)."""
