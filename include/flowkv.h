@@ -183,7 +183,8 @@ int flowkv_allocator_stats(const flowkv_allocator* a, flowkv_alloc_stats* out);
    maximal runs with src and dst both stepping by +1 to out[0 .. *n_out), in
    logical order, `first` counting from 0.
    ERANGE: an ID outside its pool; EDUP: an ID repeated within src_ids or
-   within dst_ids; ECAP: more than `cap` runs (*n_out = runs needed);
+   within dst_ids; ECAP: more than `cap` runs (*n_out = runs needed, out
+   untouched);
    EINVAL: NULL pointers (arrays may be NULL when n_blocks == 0), negative
    sizes.  The run count is at most n_blocks. */
 int flowkv_plan(const int32_t* src_ids, const int32_t* dst_ids, int32_t n_blocks,
