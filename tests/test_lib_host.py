@@ -369,6 +369,57 @@ def test_plan_repeats_capacities_and_reuse_after_errors():
     assert as_tuples(fk.flowkv_plan([0, 1, 2], [5, 6, 7], P, P)) == [(0, 5, 3)]
 
 
+def test_plan_batch_repeats_across_and_within_requests():
+    """A batch may repeat a sender block across requests (a shared prefix)
+    but not within one, and may not repeat a receiver block anywhere.  On
+    seeded batches built from runs of IDs the planner either matches the
+    oracle's per-request plans or names the first offending position: the
+    receiver list over the whole batch is checked first, then each
+    request's sender list."""
+    g = np.random.default_rng(41)
+    P = 400
+    outcomes = {"ok": 0, "receiver": 0, "sender": 0}
+    for case in range(300):
+        tables = []
+        for _ in range(int(g.integers(1, 6))):
+            n = int(g.integers(0, 25))
+            def ids():
+                out, x = [], int(g.integers(0, P))
+                while len(out) < n:
+                    if g.random() < 0.3:
+                        x = int(g.integers(0, P))
+                    out.append(x % P)
+                    x += 1
+                return out
+            tables.append((ids(), ids()))
+        off = np.concatenate(([0], np.cumsum([len(s) for s, _ in tables]))).astype(np.int64)
+        S = [x for s, _ in tables for x in s]
+        D = [x for _, d in tables for x in d]
+        rd = first_repeat(D)
+        rs = None
+        for r, (sr, _) in enumerate(tables):
+            k = first_repeat(sr)
+            if k is not None:
+                rs = int(off[r]) + k
+                break
+        if rd is None and rs is None:
+            segs = fk.flowkv_plan_batch(off, S, D, P, P)
+            want = oracle.plan_batch_ref(tables)
+            assert as_tuples(segs) == [w[:3] for w in want], case
+            assert fk.plan_total_blocks(segs) == len(S)
+            outcomes["ok"] += 1
+            continue
+        with pytest.raises(fk.FlowKVError) as e:
+            fk.flowkv_plan_batch(off, S, D, P, P)
+        assert e.value.code == fk.EDUP, case
+        pos, ids, side = (rd, D, "receiver") if rd is not None else (rs, S, "sender")
+        msg = fk.lib().flowkv_last_error().decode()
+        assert msg.startswith(side) and f"block {ids[pos]} repeated (position {pos})" in msg, \
+            (case, msg, side, pos)
+        outcomes[side] += 1
+    assert min(outcomes.values()) >= 20, outcomes
+
+
 def test_plan_errors():
     P = 16
     cases = [((P,), (0,), fk.ERANGE), ((0,), (-1,), fk.ERANGE), ((1, 1), (2, 3), fk.EDUP),
