@@ -9,9 +9,10 @@ random, which gives 255 runs.  A step is one pass of the hot path for that
 request:
   1. bidirectional segment alignment of the sender's and receiver's block
      lists (host),
-  2. the plan goes to the device: in the kernel's arguments when it has at
-     most 64 runs, else staged through a ring of pinned buffers (one small
-     copy on a side stream, overlapping the previous kernel),
+  2. the plan goes to the device: in the kernel's arguments when it fits
+     there (64 runs, or 300 between block-major pools in the planner's
+     form), else staged through a ring of pinned buffers (one small copy on
+     a side stream, overlapping the previous kernel),
   3. one kernel launch moves every run's K and V of all 32 layers.
 With --dst-policy segment the receiver's segment allocator also runs inside
 every step: it places the request's 813 blocks in the 30%-occupied pool (43
@@ -30,7 +31,8 @@ transfer kernel's own launches (events around each launch -- or, with
 --layerwise, around each step's per-layer launches -- on their stream)
 against the 8 TB/s HBM peak with 2x payload (read + write) of traffic;
 `cpu_baseline` is the oracle (numpy, one thread) moving the same blocks on the
-host.
+host.  The timed launches are bracketed by HIP events made for timing only
+(see TimingEvent).
 """
 
 from __future__ import annotations
@@ -54,6 +56,81 @@ METRIC = "effective KV transfer GB/s (% of HBM peak); ms per 13k-token request t
 KERNEL_SRC = os.path.join(ROOT, "paper_2504_03775_amd", "csrc", "flowkv_transfer.hip")
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "kv_segment_copy_llama3-8b-13k_pmc.txt")
 ATTN_SRC = os.path.join(ROOT, "paper_2504_03775_amd", "csrc", "flowkv_attention.hip")
+
+# hipEventDisableSystemFence (hip_runtime_api.h): recording the event skips
+# the system-scope fence (an L2 write-back and invalidation) that an ordinary
+# event adds after the work it follows
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
+_HIP_RT = []
+
+
+def _hip_runtime():
+    """The HIP runtime torch loaded (one per process), with the event calls."""
+    if not _HIP_RT:
+        paths = sorted({ln.split()[-1] for ln in open("/proc/self/maps")
+                        if "libamdhip64" in ln})
+        if len(paths) != 1:
+            raise RuntimeError(f"expected one HIP runtime in the process, found {paths}")
+        lib = ctypes.CDLL(paths[0])
+        lib.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+        lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                            ctypes.c_void_p]
+        lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        _HIP_RT.append(lib)
+    return _HIP_RT[0]
+
+
+class TimingEvent:
+    """A HIP event for timing only, with torch.cuda.Event's record() and
+    elapsed_time().  It is created with hipEventDisableSystemFence: an
+    ordinary event's completion fence writes back and invalidates the caches
+    between back-to-back kernels, which measurably lengthens both the step
+    and the interval the events bracket (about 3 us per 0.55 ms step)."""
+
+    def __init__(self):
+        self._rt = _hip_runtime()
+        self._h = ctypes.c_void_p()
+        rc = self._rt.hipEventCreateWithFlags(ctypes.byref(self._h),
+                                              HIP_EVENT_DISABLE_SYSTEM_FENCE)
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags returned {rc}")
+
+    def record(self, stream=None):
+        import torch
+
+        s = stream if stream is not None else torch.cuda.current_stream()
+        rc = self._rt.hipEventRecord(self._h, ctypes.c_void_p(s.cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord returned {rc}")
+
+    def elapsed_time(self, end: "TimingEvent") -> float:
+        ms = ctypes.c_float()
+        rc = self._rt.hipEventElapsedTime(ctypes.byref(ms), self._h, end._h)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime returned {rc}")
+        return ms.value
+
+    def __del__(self):
+        h, self._h = getattr(self, "_h", None), None
+        if h:
+            self._rt.hipEventDestroy(h)
+
+
+TIMING = {"events": "hip, system fence disabled"}
+
+
+def timing_pairs(k: int):
+    """k (start, end) timing-event pairs: TimingEvent, or torch's events
+    where the runtime refuses the flag (TIMING says which)."""
+    import torch
+
+    try:
+        return [(TimingEvent(), TimingEvent()) for _ in range(k)]
+    except (RuntimeError, OSError, AttributeError) as e:
+        TIMING["events"] = f"torch ({e})"
+        return [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for _ in range(k)]
 ATTN_PMC_SUMMARY = {
     "batch": os.path.join(ROOT, "profiles", "decode_attn_llama3-8b-batch32_pmc.txt"),
     "70b": os.path.join(ROOT, "profiles", "decode_attn_llama3-70b-tp8-share_pmc.txt"),
@@ -216,8 +293,7 @@ def bench_attention(args):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.steps)]
+    evs = timing_pairs(args.steps)
     gc.collect()
     gc.disable()
     t0 = time.perf_counter()
@@ -274,6 +350,7 @@ def bench_attention(args):
                    "block_size": geom.block_size, "kv_dtype": "bf16",
                    "layout": f"{args.layout}-major", "layer": layer, "split_tokens": split},
         "kernel_ms_avg": round(ms, 4),
+        "timing_events": TIMING["events"],
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic_from_profile(ATTN_PMC_SUMMARY.get(args.attn_workload)
@@ -749,8 +826,7 @@ def main():
     torch.cuda.synchronize()
 
     # ---- timed region -----------------------------------------------------------
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.steps)]
+    evs = timing_pairs(args.steps)
     # Python's cyclic garbage collector is run before and kept off during the
     # timed steps (as timeit does): a full collection of the interpreter's
     # heap can stall the host for tens of milliseconds mid-loop
@@ -788,7 +864,7 @@ def main():
             scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
             for _ in range(10):
                 scratch.fill_(1)
-                e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                e = timing_pairs(1)[0]
                 step(e)
                 torch.cuda.synchronize()
                 flushed.append(e[0].elapsed_time(e[1]))
@@ -869,8 +945,7 @@ def main():
             spot_check(table_alt())
             for _ in range(args.warmup):
                 step(fns=fns)
-            evs_alt = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                       for _ in range(args.steps)]
+            evs_alt = timing_pairs(args.steps)
             torch.cuda.synchronize()
             gc.collect()
             gc.disable()
@@ -975,6 +1050,7 @@ def main():
         "kernel_ms_avg": round(kern_avg_ms, 4),
         "kernel_ms_p10_p50_p90": [round(float(x), 4) for x in
                                   np.percentile(np.asarray(kern_ms), [10, 50, 90])],
+        "timing_events": TIMING["events"],
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic},

@@ -124,6 +124,33 @@ def test_schedule_line_contract_on_cpu():
 
 
 @pytest.mark.gpu
+def test_timing_events_bracket_the_same_work_as_torch_events():
+    """bench.py's timing events (no system fence) measure what torch's
+    events measure: a pair nested inside a torch pair around five 1 GiB
+    copies reads at most the outer interval and at least 90% of it."""
+    import torch
+
+    import bench
+
+    a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    outer = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    inner = bench.timing_pairs(1)[0]
+    assert bench.TIMING["events"].startswith("hip"), bench.TIMING
+    outer[0].record()
+    inner[0].record()
+    for _ in range(5):
+        b.copy_(a)
+    inner[1].record()
+    outer[1].record()
+    torch.cuda.synchronize()
+    mi, mo = inner[0].elapsed_time(inner[1]), outer[0].elapsed_time(outer[1])
+    assert 0.9 * mo <= mi <= mo * 1.01 + 0.01, (mi, mo)
+
+
+@pytest.mark.gpu
 def test_attention_line_contract():
     j = run_bench("--op", "attention", "--attn-workload", "70b", "--steps", "3", "--warmup", "1",
                   "--no-context", "--no-cpu-baseline")
