@@ -16,7 +16,6 @@ from hypothesis import given, settings, strategies as st
 
 import oracle
 from paper_2504_03775_amd import flowkv as fk
-from workloads import churn_ops, replay, occupied_blocks, SEED_OCCUPANCY
 from workloads import recipes
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))

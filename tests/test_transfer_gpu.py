@@ -17,7 +17,7 @@ import torch
 
 import oracle
 from paper_2504_03775_amd import flowkv as fk
-from workloads import TINY, LLAMA3_8B, Geometry, random_table, recipes
+from workloads import TINY, LLAMA3_8B, Geometry, recipes
 from tests.gpu_helpers import (BM, LM, check_full_pool, check_sampled, device_pool,
                                download_all, first_mismatch, host_equal, plan_tables,
                                run_transfer)
