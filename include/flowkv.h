@@ -300,7 +300,8 @@ int flowkv_decode_attention_workspace(int32_t n_req, int32_t q_heads, int32_t he
    head_dim 64 or 128; q_heads / kv_heads in {1, 2, 4, 8}; split_tokens 0 =
    the default rule (flowkv_decode_attention_split), else
    1..FLOWKV_ATTN_MAX_SPLIT.  Two launches on hip_stream.  At most 65,535
-   requests and 65,535 splits (ceil(max_seq_len / split_tokens)) per call.
+   requests and 65,535 splits (ceil(max_seq_len / split_tokens)) per call,
+   and max_blocks x block_size at most 2^31 - 1 tokens.
    EINVAL for bad shapes or pointers, ECAP for a short workspace. */
 int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer, const void* q_dev,
                             int32_t n_req, int32_t q_heads, int32_t kv_heads,

@@ -856,6 +856,11 @@ extern "C" int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer,
     return fail(FLOWKV_EINVAL, "block stride of %lld bytes: need under 4 GiB", (long long)stride);
   if (n_req < 0 || max_blocks < 0 || max_seq_len < 0)
     return fail(FLOWKV_EINVAL, "negative sizes");
+  // token indices are 32-bit in the kernels: a table row addresses at most
+  // 2^31 - 1 tokens
+  if (int64_t(max_blocks) * bs > INT32_MAX)
+    return fail(FLOWKV_EINVAL, "max_blocks %d x block_size %lld tokens: need at most 2^31 - 1",
+                max_blocks, (long long)bs);
   if (split_tokens == 0) split_tokens = auto_split(n_req, max_seq_len);
   if (split_tokens < 1 || split_tokens > FLOWKV_ATTN_MAX_SPLIT)
     return fail(FLOWKV_EINVAL, "split_tokens %d: need 1..%d", split_tokens,

@@ -609,6 +609,7 @@ def test_attention_rejects_bad_arguments_without_touching_the_device():
         dict(n_req=70000),                         # past the grid's 65,535 requests
         dict(max_seq=70000, split=1),              # past the grid's 65,535 splits
         dict(max_blocks=-1), dict(q=0), dict(ws=0),
+        dict(max_blocks=1 << 27),                  # 2^27 blocks x 16 tokens: past 2^31 - 1
     ]
     for c in cases:
         assert attn(p, **c) == fk.EINVAL, c
