@@ -248,6 +248,20 @@ int flowkv_transfer_inline(const flowkv_pool* src, const flowkv_pool* dst,
                            int64_t total_blocks, const flowkv_launch_config* cfg,
                            void* hip_stream);
 
+/* Move one request (section 3.1's problem statement: K and V of request R
+   from the sender's pool to the receiver's) in one call: flowkv_plan of src_ids
+   and dst_ids (n_blocks each, host memory, pool sizes taken from the pool
+   descriptors), then flowkv_transfer_inline with that plan.  *n_runs
+   receives the plan's run count.  ECAP, with *n_runs set and nothing
+   launched, when the plan has more runs than flowkv_transfer_inline carries
+   between these pools (then plan with flowkv_plan and launch with a device
+   plan).  Errors of the planner (ERANGE, EDUP) come before any launch; the
+   others are flowkv_transfer_inline's.  n_blocks == 0 is a no-op. */
+int flowkv_transfer_request(const flowkv_pool* src, const flowkv_pool* dst,
+                            const int32_t* src_ids, const int32_t* dst_ids, int32_t n_blocks,
+                            const flowkv_launch_config* cfg, int64_t* n_runs,
+                            void* hip_stream);
+
 /* Layer-wise variant (section 4.4 and Table 3: the "FlowKV-Layerwise"
    ablation, which moves the KV cache one layer at a time, as a sender that
    streams layers while prefill still runs would).  Moves only layers

@@ -22,7 +22,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libflowkv.so")
 
-HOST_SOURCES = ["flowkv_status.cpp", "flowkv_alloc.cpp", "flowkv_plan.cpp", "flowkv_sched.cpp"]
+HOST_SOURCES = ["flowkv_status.cpp", "flowkv_alloc.cpp", "flowkv_plan.cpp", "flowkv_sched.cpp",
+                "flowkv_request.cpp"]
 HIP_SOURCES = ["flowkv_transfer.hip", "flowkv_attention.hip"]
 
 ARCH = "gfx950"

@@ -102,6 +102,10 @@ SIGNATURES = {
     "flowkv_transfer_inline": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_int64,
                                               ctypes.c_int64, ctypes.POINTER(flowkv_launch_config),
                                               ctypes.c_void_p]),
+    "flowkv_transfer_request": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_void_p,
+                                               ctypes.c_int32,
+                                               ctypes.POINTER(flowkv_launch_config), _I64P,
+                                               ctypes.c_void_p]),
     "flowkv_transfer_layers": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_int64,
                                               ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                               ctypes.POINTER(flowkv_launch_config),
@@ -483,6 +487,24 @@ def flowkv_transfer_inline(src: KVPool, dst: KVPool, segs: np.ndarray, total_blo
                                        _ptr(segs), len(segs), total_blocks,
                                        ctypes.byref(cfg), ctypes.c_void_p(_stream_handle(stream))),
            "flowkv_transfer_inline")
+
+
+def flowkv_transfer_request(src: KVPool, dst: KVPool, src_ids, dst_ids, threads: int = 0,
+                            unroll: int = 0, grid: int = 0, cache: int = 0, order: int = 0,
+                            stream=None) -> int:
+    """Plan one request and enqueue its copy with the plan in the kernel
+    arguments, in one library call; returns the plan's run count.  Raises
+    FlowKVError(ECAP) when the plan does not fit there (``inline_capacity``)."""
+    s, d = _i32(src_ids), _i32(dst_ids)
+    if s.size != d.size:
+        raise ValueError("sender and receiver lists differ in length")
+    cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
+    n = ctypes.c_int64()
+    _check(_lib.flowkv_transfer_request(ctypes.byref(src.desc), ctypes.byref(dst.desc),
+                                        _ptr(s), _ptr(d), s.size, ctypes.byref(cfg),
+                                        ctypes.byref(n), ctypes.c_void_p(_stream_handle(stream))),
+           "flowkv_transfer_request")
+    return n.value
 
 
 def flowkv_transfer_layers(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_blocks: int,

@@ -571,6 +571,34 @@ def test_transfer_rejects_bad_pools_without_touching_the_device():
     assert xfer(good_src, good_dst, n_segs=-1) == fk.EINVAL
 
 
+def test_transfer_request_rejects_before_any_device_call():
+    """flowkv_transfer_request: NULL pools, a negative count, the planner's
+    ERANGE and EDUP, and ECAP past the inline capacity (run count reported)
+    all return before anything is launched; zero blocks is a no-op."""
+    lib = fk.lib()
+    bm = pool(layout=1, L=2, B=1000)                             # 16 MB at 1 MiB
+    bm2 = pool(layout=1, L=2, B=1000, bases=(1 << 30,))
+    lm = pool(layout=0, L=2, B=1000, bases=(1 << 28, 1 << 29))
+
+    def req(src, dst, S, D, n=None):
+        S, D = np.ascontiguousarray(S, np.int32), np.ascontiguousarray(D, np.int32)
+        k = ctypes.c_int64(-1)
+        rc = lib.flowkv_transfer_request(src and ctypes.byref(src), dst and ctypes.byref(dst),
+                                         S.ctypes.data, D.ctypes.data,
+                                         len(S) if n is None else n, None, ctypes.byref(k), None)
+        return rc, k.value
+
+    assert req(None, bm2, [0], [0])[0] == fk.EINVAL
+    assert req(bm, bm2, [0], [0], n=-1)[0] == fk.EINVAL
+    assert req(bm, bm2, [1000], [0])[0] == fk.ERANGE
+    assert req(bm, bm2, [1, 1], [2, 3])[0] == fk.EDUP
+    assert req(bm, bm2, [], []) == (fk.OK, 0)
+    assert req(bm, bm, [], [])[0] == fk.EINVAL                      # overlapping pools
+    stride2 = 2 * np.arange(301)
+    assert req(bm, bm2, stride2, stride2 + 1) == (fk.ECAP, 301)      # block-major: 300 fit
+    assert req(bm, lm, np.arange(65) * 2, np.arange(65) * 2) == (fk.ECAP, 65)   # else 64
+
+
 def test_abi_check_program_is_built_and_runs_without_python():
     """The build step also builds tests/native/abi_transfer, which uses the
     library through the C ABI alone; its dynamic links resolve, and without

@@ -432,6 +432,48 @@ def test_compact_inline_plans_against_oracle(seed):
     assert host_equal(got, h_dst), first_mismatch(got, h_dst)
 
 
+@pytest.mark.parametrize("sl,dl", [(BM, BM), (LM, LM), (LM, BM)], ids=lambda x: NAMES[x])
+def test_transfer_request_plans_and_moves_one_request(sl, dl):
+    """flowkv_transfer_request (plan and launch in one call) on a request
+    whose lists are runs of consecutive IDs with random breaks: the receiver
+    pool equals the oracle's, byte for byte, and the run count is the
+    planner's.  A plan past the inline capacity raises ECAP and moves
+    nothing."""
+    geom = Geometry("req", 4, 2, 64, 16, "bfloat16")
+    B = 700                        # room for the stride-2 lists of 301 blocks below
+    g = np.random.default_rng(77 + sl * 2 + dl)
+    def table(n):
+        out, x, used = [], int(g.integers(0, B)), set()
+        while len(out) < n:
+            if g.random() < 0.08 or x >= B or x in used:
+                x = int(g.integers(0, B))
+                continue
+            out.append(x)
+            used.add(x)
+            x += 1
+        return np.asarray(out, dtype=np.int32)
+    S, D = table(200), table(200)
+    want_runs = len(fk.flowkv_plan(S, D, B, B))
+    src = device_pool(geom, sl, B, 5)
+    dst = device_pool(geom, dl, B, 6)
+    cap = fk.inline_capacity(src, dst)
+    assert want_runs <= cap, (want_runs, cap)
+    h_src, h_dst = download_all(src), download_all(dst)
+    say(f"request {NAMES[sl]}->{NAMES[dl]}: {len(S)} blocks, {want_runs} runs, capacity {cap}")
+    assert fk.flowkv_transfer_request(src, dst, S, D) == want_runs
+    torch.cuda.synchronize()
+    oracle.transfer_fast(h_src, h_dst, S, D)
+    after = download_all(dst)
+    assert host_equal(after, h_dst)
+    # past the capacity: ECAP with the run count, and the receiver untouched
+    k = cap + 1
+    with pytest.raises(fk.FlowKVError) as e:
+        fk.flowkv_transfer_request(src, dst, 2 * np.arange(k), 2 * np.arange(k) + 1)
+    assert e.value.code == fk.ECAP
+    torch.cuda.synchronize()
+    assert host_equal(download_all(dst), after)
+
+
 def test_inline_plan_at_the_limit_equals_device_plan():
     """64 one-block runs (the inline limit) at the 8B geometry: the inline and
     the device-memory plan give the same receiver pool, and match the oracle."""
