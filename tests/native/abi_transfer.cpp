@@ -6,12 +6,14 @@
 // segment policy on a pool with every fifth block held; the receiver's uses a
 // seeded shuffled free list.  Request A (30 blocks) is planned, its plan
 // copied to the device and moved with flowkv_transfer; request B (12 blocks)
-// is moved with flowkv_transfer_inline from the host plan.  Two error paths
-// are checked on the way.
+// is moved with flowkv_transfer_inline from the host plan; request C (10
+// blocks) is planned and moved in one flowkv_transfer_request call.  Two
+// error paths are checked on the way.
 //
 // Writes to <out_dir>: src.bin (the sender pool), dst_before.bin and
 // dst_after.bin (the receiver pool around the two transfers) and tables.txt
-// (geometry, then the sender and receiver block lists of A and B).  A test
+// (geometry and run counts, then the sender and receiver block lists of A, B
+// and C).  A test
 // compares dst_after with the oracle's result on src and dst_before.
 // Prints "abi ok" and exits 0 when every call returned what it should.
 //
@@ -126,11 +128,13 @@ int main(int argc, char** argv) {
   std::vector<int32_t> held;
   for (int32_t b = 0; b < kSrcBlocks; b += 5) held.push_back(b);
   fk_ok(flowkv_mark_used(sa, held.data(), int32_t(held.size())), "flowkv_mark_used");
-  std::vector<int32_t> SA(30), DA(30), SB(12), DB(12);
+  std::vector<int32_t> SA(30), DA(30), SB(12), DB(12), SC(10), DC(10);
   fk_ok(flowkv_alloc(sa, 30, SA.data()), "alloc sender A");
   fk_ok(flowkv_alloc(da, 30, DA.data()), "alloc receiver A");
   fk_ok(flowkv_alloc(sa, 12, SB.data()), "alloc sender B");
   fk_ok(flowkv_alloc(da, 12, DB.data()), "alloc receiver B");
+  fk_ok(flowkv_alloc(sa, 10, SC.data()), "alloc sender C");
+  fk_ok(flowkv_alloc(da, 10, DC.data()), "alloc receiver C");
 
   hipStream_t stream;
   hip_ok(hipStreamCreate(&stream), "hipStreamCreate");
@@ -154,6 +158,11 @@ int main(int argc, char** argv) {
   fk_ok(flowkv_transfer_inline(&src, &dst, pb.data(), int64_t(pb.size()), 12, nullptr, stream),
         "flowkv_transfer_inline");
 
+  // request C: planned and launched in one call
+  int64_t runs_c = -1;
+  fk_ok(flowkv_transfer_request(&src, &dst, SC.data(), DC.data(), 10, nullptr, &runs_c, stream),
+        "flowkv_transfer_request");
+
   hip_ok(hipStreamSynchronize(stream), "hipStreamSynchronize");
   std::vector<uint8_t> dst_after(dst_bytes);
   hip_ok(hipMemcpy(dst_after.data(), dst_dev, dst_bytes, hipMemcpyDeviceToHost),
@@ -164,12 +173,15 @@ int main(int argc, char** argv) {
   write_file(dir + "/dst_after.bin", dst_after.data(), dst_bytes);
   FILE* f = std::fopen((dir + "/tables.txt").c_str(), "w");
   if (!f) die("write", "tables.txt");
-  std::fprintf(f, "%d %d %d %d %d %zu %zu\n", kLayers, kBlockSize, kKvHeads * kHeadDim * kElem,
-               kSrcBlocks, kDstBlocks, pa.size(), pb.size());
+  std::fprintf(f, "%d %d %d %d %d %zu %zu %lld\n", kLayers, kBlockSize,
+               kKvHeads * kHeadDim * kElem, kSrcBlocks, kDstBlocks, pa.size(), pb.size(),
+               (long long)runs_c);
   write_list(f, "SA", SA);
   write_list(f, "DA", DA);
   write_list(f, "SB", SB);
   write_list(f, "DB", DB);
+  write_list(f, "SC", SC);
+  write_list(f, "DC", DC);
   std::fclose(f);
 
   hip_ok(hipStreamDestroy(stream), "hipStreamDestroy");
@@ -178,6 +190,6 @@ int main(int argc, char** argv) {
   hip_ok(hipFree(dst_dev), "hipFree receiver pool");
   flowkv_allocator_destroy(sa);
   flowkv_allocator_destroy(da);
-  std::printf("abi ok: %zu and %zu runs moved\n", pa.size(), pb.size());
+  std::printf("abi ok: %zu, %zu and %lld runs moved\n", pa.size(), pb.size(), (long long)runs_c);
   return 0;
 }
