@@ -14,7 +14,9 @@
  *                     receiving side together (section 3.3; Figure 3 caption);
  *   flowkv_transfer -- one device launch that copies every run of every layer's
  *                     K and V, in the per-layer layout (L, 2, B, H) or the
- *                     block-major layout (B, L, 2, H) of Eq. 5, on one GPU.
+ *                     block-major layout (B, L, 2, H) of Eq. 5, on one GPU;
+ *                     flowkv_transfer_request plans and launches one request
+ *                     in a single call.
  *
  * Beside them: flowkv_decode_attention*, the paged decode attention that
  * reads either layout (the PagedAttention kernel section 3.3 adapts), and
@@ -26,7 +28,7 @@
  *     throws across the ABI.  flowkv_strerror() names a code;
  *     flowkv_last_error() gives the calling thread's last detailed message.
  *   - On error, output arguments are left untouched, except *n_out of the
- *     planners on FLOWKV_ECAP.
+ *     planners and *n_runs of flowkv_transfer_request on FLOWKV_ECAP.
  *   - The caller owns every buffer.  The library allocates no device memory and
  *     keeps no pointer after a call returns, except inside an allocator or a
  *     scheduler handle.
