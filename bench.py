@@ -154,7 +154,8 @@ WORKLOADS = {
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
-    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--gpus", type=int, default=1,
+                    help="GPUs to use: 1 only (the path runs on one device)")
     ap.add_argument("--op", choices=["transfer", "attention", "schedule", "overlap"],
                     default="transfer",
                     help="transfer: the KV transfer hot path (default); attention: one decode "
@@ -163,8 +164,8 @@ def parse():
                          "cluster model's three load mixes with fixed and load-aware roles; "
                          "overlap: the 13k request's transfer after, or layer by layer beside, "
                          "a prefill stand-in")
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=100, help="timed steps")
+    ap.add_argument("--warmup", type=int, default=10, help="untimed steps before them")
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="8b")
     ap.add_argument("--layout", choices=["block", "layer"], default="block",
                     help="pool layout of both sides: Eq. 5 block-major or per-layer")
@@ -178,13 +179,19 @@ def parse():
                          "ablation) instead of one launch for all layers")
     ap.add_argument("--staged-plan", action="store_true",
                     help="always stage the plan in device memory (no kernel-argument plans)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip timing the oracle on the host")
     ap.add_argument("--no-context", action="store_true",
                     help="skip the memcpy comparators and the flushed-cache timing")
-    ap.add_argument("--threads", type=int, default=0)
-    ap.add_argument("--unroll", type=int, default=0)
-    ap.add_argument("--grid", type=int, default=0)
-    ap.add_argument("--cache", type=int, default=0)
+    ap.add_argument("--threads", type=int, default=0,
+                    help="transfer workgroup size, 64..1024 (0 = library default)")
+    ap.add_argument("--unroll", type=int, default=0,
+                    help="16-byte vectors per thread per tile: 2, 4, 8, 16 (0 = default)")
+    ap.add_argument("--grid", type=int, default=0,
+                    help="transfer workgroups (0 = one per tile, capped per CU)")
+    ap.add_argument("--cache", type=int, default=0,
+                    help="1 plain, 2 nontemporal loads, 3 nontemporal stores, "
+                         "4 both (0 = default)")
     ap.add_argument("--order", type=int, default=0,
                     help="tile visiting order: 1 plan order, 2 blocks scattered, 3 tiles "
                          "scattered (0 = library default)")
