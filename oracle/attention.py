@@ -23,6 +23,10 @@ that key's V, with a constant V per KV head every query head returns its
 group's constant, agreement with a separate dense softmax-attention computed
 from numpy's einsum on a contiguous copy, and invariance under relabelling
 the pool's blocks.
+
+``decode_attention_scales`` returns, next to each output element, the sizes
+its rounding errors scale with in any float32 evaluation of the same sums
+(test infrastructure for setting tolerances; see its docstring).
 """
 
 from __future__ import annotations
@@ -60,6 +64,54 @@ def gather_kv(pool: HostPool, table: Sequence[int], T: int, layer: int, kv_heads
     return out
 
 
+def _weights(K: np.ndarray, qh: np.ndarray, scale: float):
+    """Scores s_t = scale * q . K_t and softmax weights p_t over tokens."""
+    s = scale * (K @ qh)
+    p = np.exp(s - s.max())
+    return s, p / p.sum()
+
+
+def decode_attention_scales(pool: HostPool, q: np.ndarray, tables, seq_lens, layer: int,
+                            kv_heads: int, head_dim: int, scale: float):
+    """decode_attention plus, per output element (r, h, d), the quantities its
+    rounding errors scale with (float64):
+
+      out  the attention output o[r, h, d] (as decode_attention);
+      w1   sum_t p_t |V_t,d|: bounds every partial sum of p_t V_t,d, so an
+           error of relative size e in each addition of those sums moves
+           o by at most about e * w1 per addition;
+      w2   sqrt(sum_t p_t^2 (V_t,d - o_d)^2): independent relative errors
+           delta_t in the weights move o by sum_t p_t delta_t (V_t,d - o_d),
+           whose spread is |delta| * w2;
+      s1   per (r, h): scale * max_t sum_d |q_d K_t,d|, the largest sum of
+           absolute products in a score, which bounds a score's rounding
+           error relative to the number of its roundings."""
+    q = np.asarray(q, dtype=np.float64)
+    n, Hq, D = q.shape
+    if D != head_dim or Hq % kv_heads:
+        raise ValueError("query shape does not match the pool's heads")
+    group = Hq // kv_heads
+    out = np.zeros((n, Hq, D))
+    w1 = np.zeros((n, Hq, D))
+    w2 = np.zeros((n, Hq, D))
+    s1 = np.zeros((n, Hq))
+    for r in range(n):
+        T = int(seq_lens[r])
+        if T < 1:
+            raise ValueError("a request needs at least one token")
+        kvr = gather_kv(pool, tables[r], T, layer, kv_heads, head_dim)
+        K, V = kvr[0], kvr[1]
+        for h in range(Hq):
+            g = h // group
+            _, p = _weights(K[:, g, :], q[r, h], scale)
+            o = p @ V[:, g, :]
+            out[r, h] = o
+            w1[r, h] = p @ np.abs(V[:, g, :])
+            w2[r, h] = np.sqrt((p ** 2) @ (V[:, g, :] - o) ** 2)
+            s1[r, h] = scale * np.max(np.abs(K[:, g, :]) @ np.abs(q[r, h]))
+    return out, w1, w2, s1
+
+
 def decode_attention(pool: HostPool, q: np.ndarray, tables, seq_lens, layer: int,
                      kv_heads: int, head_dim: int, scale: float) -> np.ndarray:
     """Decode attention of ``n`` requests, float64.
@@ -82,8 +134,6 @@ def decode_attention(pool: HostPool, q: np.ndarray, tables, seq_lens, layer: int
         K, V = kvr[0], kvr[1]
         for h in range(Hq):
             g = h // group
-            s = scale * (K[:, g, :] @ q[r, h])          # (T,)
-            p = np.exp(s - s.max())
-            p /= p.sum()
+            _, p = _weights(K[:, g, :], q[r, h], scale)
             out[r, h] = p @ V[:, g, :]
     return out

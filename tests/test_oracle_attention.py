@@ -162,3 +162,119 @@ def test_rejects_bad_inputs():
         decode_attention(pool, np.zeros((1, 2, 8)), [[0]], [3], 0, 2, 8, 1.0)  # T > blocks
     with pytest.raises(ValueError):
         decode_attention(pool, np.zeros((1, 2, 8)), [[0]], [0], 0, 2, 8, 1.0)  # T = 0
+
+
+# ---- the GPU tests' tolerance: it rejects plausible kernel errors -----------------
+#
+# tests/attn_tolerance.py bounds |kernel - oracle| per output element from the
+# scales decode_attention_scales returns.  Here, in numpy, float32 evaluations
+# of attention stand in for kernels: two that are right (the vector pass's
+# arithmetic, and the matrix-core pass's weights carried as two bf16 parts)
+# must pass, and two with bugs a loose bound would let through must fail.
+
+from tests import attn_tolerance  # noqa: E402
+
+
+def long_request(T, hkv, hq, dh, seed):
+    """One request of T tokens on a one-layer block-major pool with N(0, 1)
+    bf16 K, V and q; returns the oracle's output and scales, K and V as
+    float32, q, and the scale."""
+    from oracle.attention import decode_attention_scales, gather_kv
+
+    rng = np.random.default_rng(seed)
+    bs, B = 16, -(-T // 16)
+    pool = HostPool.zeros(BLOCK_MAJOR, 1, B, bs, hkv * dh * 2)
+    pool.buffers[0].view(np.uint16)[:] = to_bf16(rng.standard_normal(pool.buffers[0].size // 2))
+    q = from_bf16(to_bf16(rng.standard_normal((1, hq, dh))))
+    scale = 1 / np.sqrt(dh)
+    table = list(range(B))
+    out, w1, w2, s1 = decode_attention_scales(pool, q, [table], [T], 0, hkv, dh, scale)
+    kv = gather_kv(pool, table, T, 0, hkv, dh).astype(np.float32)
+    return out, w1, w2, s1, kv, q, scale
+
+
+def float32_attention(kv, q, scale, hq, hkv, weights="f32", drop=None):
+    """Attention of one request evaluated in float32: scores, exp2 weights
+    against the largest score, their sum L, and sum_t w_t V_t / L with the
+    weights w_t taken as float32 ('f32'), as bf16(p) + bf16(p - bf16(p))
+    ('hi+lo'), or as bf16(p) alone ('hi').  `drop` leaves the 32 tokens from
+    that index out of the weighted sum (a skipped tile)."""
+    K, V = kv[0], kv[1]
+    o = np.zeros((1, hq, K.shape[2]))
+    for h in range(hq):
+        g = h // (hq // hkv)
+        s = (K[:, g, :] @ q[0, h].astype(np.float32)) * np.float32(scale * np.log2(np.e))
+        p = np.exp2(s - s.max()).astype(np.float32)
+        L = p.sum(dtype=np.float32)
+        if drop is not None:
+            p[drop:drop + 32] = 0
+        hi = from_bf16(to_bf16(p)).astype(np.float32)
+        if weights == "f32":
+            num = p @ V[:, g, :]
+        elif weights == "hi":
+            num = hi @ V[:, g, :]
+        else:
+            lo = from_bf16(to_bf16(p - hi)).astype(np.float32)
+            num = (hi @ V[:, g, :]).astype(np.float32) + (lo @ V[:, g, :]).astype(np.float32)
+        o[0, h] = num.astype(np.float32) / L
+    return o
+
+
+HQ, HKV, DH = 8, 1, 128     # the matrix-core pass's shape (one 70B TP=8 share)
+
+
+@pytest.mark.parametrize("T", [50, 300, 4097, 20000])
+def test_tolerance_accepts_float32_evaluations(T):
+    out, w1, w2, s1, kv, q, scale = long_request(T, HKV, HQ, DH, T)
+    for weights, mc in (("f32", False), ("hi+lo", True)):
+        got = float32_attention(kv, q, scale, HQ, HKV, weights)
+        attn_tolerance.check(got, out, w1, w2, s1, [T], 256, mc)
+
+
+@pytest.mark.parametrize("T", [300, 4097, 20000])
+def test_tolerance_rejects_weights_carried_as_bf16_alone(T):
+    """Dropping the low bf16 part of the matrix-core pass's weights (errors
+    near 1e-4 at these lengths) fails the bound."""
+    out, w1, w2, s1, kv, q, scale = long_request(T, HKV, HQ, DH, T)
+    got = float32_attention(kv, q, scale, HQ, HKV, "hi")
+    tol = attn_tolerance.tolerance(w1, w2, s1, [T], 256, True)
+    assert np.any(np.abs(got - out) > tol)
+    with pytest.raises(AssertionError):
+        attn_tolerance.check(got, out, w1, w2, s1, [T], 256, True)
+
+
+def test_tolerance_rejects_a_skipped_tile_in_every_head():
+    """Leaving one interior 32-token tile out of a 32,000-token request
+    fails the bound in every query head."""
+    T = 32000
+    out, w1, w2, s1, kv, q, scale = long_request(T, HKV, HQ, DH, 7)
+    got = float32_attention(kv, q, scale, HQ, HKV, "hi+lo", drop=16000)
+    tol = attn_tolerance.tolerance(w1, w2, s1, [T], 1024, True)
+    bad = np.abs(got - out) > tol
+    assert bad.any(axis=2).all(), bad.any(axis=2)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_error_scales_closed_forms(layout):
+    """decode_attention_scales returns decode_attention's output and, for one
+    token, w1 = |V|, w2 = 0 and s1 = scale * sum |q K|; for any request
+    |o| <= w1 (a weighted mean of V under weights summing to one)."""
+    from oracle.attention import decode_attention_scales
+
+    rng = np.random.default_rng(8)
+    L, B, bs, hkv, dh, hq = 2, 9, 4, 2, 8, 4
+    kv1 = to_bf16(rng.standard_normal((2, 1, hkv, dh)))
+    kvT = to_bf16(rng.standard_normal((2, 13, hkv, dh)))
+    tables = [[6], [2, 0, 8, 5]]
+    pool = build_pool(layout, L, B, bs, hkv, dh, 1, tables, [kv1, kvT])
+    q = from_bf16(to_bf16(rng.standard_normal((2, hq, dh))))
+    out, w1, w2, s1 = decode_attention_scales(pool, q, tables, [1, 13], 1, hkv, dh, 0.3)
+    assert np.array_equal(out, decode_attention(pool, q, tables, [1, 13], 1, hkv, dh, 0.3))
+    V1, K1 = from_bf16(kv1[1, 0]), from_bf16(kv1[0, 0])
+    for h in range(hq):
+        g = h // (hq // hkv)
+        assert np.array_equal(w1[0, h], np.abs(V1[g]))
+        assert np.all(w2[0, h] == 0)
+        assert s1[0, h] == pytest.approx(0.3 * np.abs(K1[g]) @ np.abs(q[0, h]), rel=1e-15)
+    assert np.all(np.abs(out) <= w1 * (1 + 1e-12))
+    assert np.all(w2[1] > 0)
