@@ -10,8 +10,11 @@
 //
 // Decode attention reads every cached K and V element once and does about
 // G flops per byte (G = Hq / Hkv query heads per KV head): it is HBM-bound,
-// so it runs on the vector units (no MFMA), and the work per token is kept
-// small enough that the loads stay the limit.
+// and the work per token is kept small enough that the loads stay the limit.
+// Two forms of pass 1 serve it: a vector-unit pass (below) for head_dim 64
+// and for up to 4 query heads per KV head, and a matrix-core pass
+// (decode_attn_split_mfma, further down) for 8 query heads per KV head at
+// head_dim 128, where the vector pass reaches its ALU limit.
 // Work split (flash-decoding style):
 //   pass 1: one workgroup per (KV head, token split, request).  A token's
 //           head vector (Dh bf16) is read by one 16-lane DPP row, Dh/16
@@ -448,6 +451,16 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split_mfma(const AttnArg
   constexpr int kTile = 32;                      // tokens per wave step
   constexpr int kVBytes = 8 * 1024;              // LDS bytes of a wave's V tile
   constexpr int kStep = kWaves * kTile;          // tokens per workgroup step
+  // What issue() puts in flight for one tile: each lane follows kLaneTokens
+  // tokens (16 apart); a token's head vector (kDh bf16) is read by the 4 lanes
+  // of one MFMA column group, 16 bytes each per instruction, so kTokLoads
+  // instructions per token for K (into registers) and as many for V (into
+  // LDS).  Every one of them counts once against the vector-memory counter.
+  constexpr int kLaneTokens = kTile / 16;
+  constexpr int kTokLoads = kDh * 2 / (4 * 16);
+  constexpr int kIssueVm = kLaneTokens * kTokLoads * 2;
+  static_assert(kLaneTokens == 2 && kTokLoads == 4, "issue() is written for 2 x 4 loads");
+  static_assert(kIssueVm < 64, "the wait count must fit the 6-bit vector-memory counter");
   static_assert(kG == 4 || kG == 8, "matrix-core pass for 4 or 8 heads per KV head");
   const int g = blockIdx.x, split = blockIdx.y, r = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, ln = tid & 63;
@@ -494,9 +507,9 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split_mfma(const AttnArg
   kbase += g * kDh * 2 + 16 * q4;
 
   // each lane follows two tokens of its wave's tile: 16 gg + c16
-  int tok[2], bi[2], sl[2];
+  int tok[kLaneTokens], bi[kLaneTokens], sl[kLaneTokens];
 #pragma unroll
-  for (int gg = 0; gg < 2; ++gg) {
+  for (int gg = 0; gg < kLaneTokens; ++gg) {
     tok[gg] = t0 + wave * kTile + 16 * gg + c16;
     bi[gg] = tok[gg] / bs - b0;
     sl[gg] = tok[gg] % bs;
@@ -525,14 +538,15 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split_mfma(const AttnArg
   }
   __syncthreads();
 
-  u32x4 kp[2][4];
-  bool live[2];
+  u32x4 kp[kLaneTokens][kTokLoads];
+  bool live[kLaneTokens];
   // K of the lane's two tokens into registers, V into LDS buffer vbuf
   // (branch-free: a token past the end or outside the pool reads the pool's
-  // first slot and is masked), then the bookkeeping advances one step
+  // first slot and is masked), then the bookkeeping advances one step.
+  // Exactly kIssueVm vector-memory instructions, no other.
   auto issue = [&](uint8_t* vbuf) {
 #pragma unroll
-    for (int gg = 0; gg < 2; ++gg) {
+    for (int gg = 0; gg < kLaneTokens; ++gg) {
       const bool in = tok[gg] < t1;
       const int b = s_blk[in ? bi[gg] : 0];
       live[gg] = in && b >= 0 && b < a.pool_blocks;
@@ -543,11 +557,12 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split_mfma(const AttnArg
       // and the next one the other half; with nontemporal loads the line
       // was often gone in between (9% more HBM traffic, measured)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < kTokLoads; ++i) {
         kp[gg][i] = *(const gvec4*)(kp0 + 64 * i);
         __builtin_amdgcn_global_load_lds(
             (const __attribute__((address_space(1))) void*)(kp0 + voff + 64 * i),
-            (__attribute__((address_space(3))) void*)(vbuf + (gg * 4 + i) * 1024), 16, 0, 0);
+            (__attribute__((address_space(3))) void*)(vbuf + (gg * kTokLoads + i) * 1024), 16, 0,
+            0);
       }
       tok[gg] += kStep;
       bi[gg] += step_q;
@@ -617,17 +632,18 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split_mfma(const AttnArg
     }
     __builtin_amdgcn_wave_barrier();
 
-    // this tile's V is in LDS once every load but the next tile's 16 has
-    // returned; masked tokens' rows are then zeroed (their weight is 0, and
-    // 0 x a stale NaN would not be)
-    asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+    // this tile's V is in LDS once every load but the next tile's kIssueVm
+    // has returned; masked tokens' rows are then zeroed (their weight is 0,
+    // and 0 x a stale NaN would not be)
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kIssueVm) : "memory");
     if (!live_t[0] || !live_t[1]) {
 #pragma unroll
       for (int gg = 0; gg < 2; ++gg)
         if (!live_t[gg])
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            *reinterpret_cast<u32x4*>(my_v + (gg * 4 + i) * 1024 + ln * 16) = u32x4{0, 0, 0, 0};
+          for (int i = 0; i < kTokLoads; ++i)
+            *reinterpret_cast<u32x4*>(my_v + (gg * kTokLoads + i) * 1024 + ln * 16) =
+                u32x4{0, 0, 0, 0};
     }
     asm volatile("" ::: "memory");
     // A operand: P[head c16][k = 8 q4 + e], token 4 e + q4, split in two bf16
