@@ -99,7 +99,15 @@ typedef struct flowkv_allocator flowkv_allocator; /* opaque, host memory only */
    dst_block on the receiver, all stepping by one together.  `first` is the
    run's position in the plan's block order: the sum of n_blocks over all
    earlier records of the same plan (a request's or a batch's), so a plan's
-   records tile [0, total blocks) in order.  16 bytes, 16-byte aligned. */
+   records tile [0, total blocks) in order.  16 bytes, 16-byte aligned.
+
+   The fourth field is `first`, not the index of the request a batch record
+   belongs to: the kernel finds the run that holds a block by searching
+   `first`, and the request index follows from it.  Runs never cross
+   requests, so with flowkv_plan_batch's offsets the record belongs to the
+   request r with offsets[r] <= first < offsets[r + 1] -- the last r with
+   offsets[r] <= first, which skips requests with no blocks -- and covers its
+   blocks first - offsets[r] .. + n_blocks - 1. */
 typedef struct flowkv_segment {
   int32_t src_block;
   int32_t dst_block;
@@ -212,6 +220,10 @@ int flowkv_plan_batch(int32_t n_req, const int64_t* offsets,
    the run's blocks from `src` to `dst`.  segs_dev is device memory holding a
    plan made by flowkv_plan/flowkv_plan_batch for pools of these sizes;
    total_blocks is the plan's block count (last record's first + n_blocks).
+   It is an argument because the launch is sized by it (a fixed number of
+   tiles per block) before any record is read, and the records are in
+   device memory, which the host could read back only with a synchronising
+   copy; the caller holds the host plan it came from.
    The caller keeps segs_dev and both pools alive until the stream passes the
    kernel.  Asynchronous: returns once the launch is enqueued.  n_segs == 0 or
    total_blocks == 0 is a no-op.

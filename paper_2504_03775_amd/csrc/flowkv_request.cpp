@@ -31,6 +31,8 @@ extern "C" int flowkv_transfer_request(const flowkv_pool* src, const flowkv_pool
                 "these pools", (long long)k, (long long)cap);
   }
   if (rc) return rc;
-  *n_runs = k;
-  return flowkv_transfer_inline(src, dst, runs, k, n_blocks, cfg, hip_stream);
+  // *n_runs is an output: written on success only (and on ECAP above)
+  const int rl = flowkv_transfer_inline(src, dst, runs, k, n_blocks, cfg, hip_stream);
+  if (rl == FLOWKV_OK) *n_runs = k;
+  return rl;
 }

@@ -378,6 +378,11 @@ def flowkv_plan_batch(offsets, src_ids, dst_ids, src_pool_blocks: int,
     s, d = _i32(src_ids), _i32(dst_ids)
     if s.size != d.size:
         raise ValueError("sender and receiver lists differ in length")
+    # the planner reads the lists up to offsets[-1]: it must be their length
+    if off.ndim != 1 or off.size < 1 or int(off[-1]) != s.size:
+        raise ValueError(f"offsets must be 1-D, n_req + 1 entries ending at the lists' length "
+                         f"{s.size}, got shape {off.shape}"
+                         + (f" ending at {int(off[-1])}" if off.ndim == 1 and off.size else ""))
     out = np.empty(max(s.size, 1), dtype=SEGMENT_DTYPE)
     n = ctypes.c_int64()
     _check(_lib.flowkv_plan_batch(off.size - 1, _ptr(off), _ptr(s), _ptr(d),
@@ -536,12 +541,7 @@ def flowkv_decode_attention_workspace(n_req: int, q_heads: int, head_dim: int,
     return b.value
 
 
-def flowkv_decode_attention(pool: KVPool, layer: int, q, block_tables, seq_lens,
-                            max_seq_len: int, scale: float, out, workspace,
-                            split_tokens: int = 0, stream=None) -> None:
-    """Decode attention of layer `layer` over `pool` (torch device tensors:
-    q (n, Hq, Dh) bf16, block_tables (n, max_blocks) int32, seq_lens (n,)
-    int32, out (n, Hq, Dh) float32, workspace uint8)."""
+def _check_attention_tensors(pool: KVPool, q, block_tables, seq_lens, out):
     import torch
 
     n, hq, dh = q.shape
@@ -551,6 +551,16 @@ def flowkv_decode_attention(pool: KVPool, layer: int, q, block_tables, seq_lens,
             raise ValueError("attention tensors: wrong dtype, layout or device")
     if tuple(out.shape) != (n, hq, dh) or block_tables.shape[0] != n or seq_lens.shape[0] != n:
         raise ValueError("attention tensors: shapes disagree")
+    return n, hq, dh
+
+
+def flowkv_decode_attention(pool: KVPool, layer: int, q, block_tables, seq_lens,
+                            max_seq_len: int, scale: float, out, workspace,
+                            split_tokens: int = 0, stream=None) -> None:
+    """Decode attention of layer `layer` over `pool` (torch device tensors:
+    q (n, Hq, Dh) bf16, block_tables (n, max_blocks) int32, seq_lens (n,)
+    int32, out (n, Hq, Dh) float32, workspace uint8)."""
+    n, hq, dh = _check_attention_tensors(pool, q, block_tables, seq_lens, out)
     if not workspace.is_contiguous() or workspace.device != pool.device:
         raise ValueError("attention workspace: not a contiguous tensor on the pool's device")
     _check(_lib.flowkv_decode_attention(

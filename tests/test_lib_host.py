@@ -248,6 +248,38 @@ def test_plan_batch_matches_oracle_and_first_runs_across_batch():
     assert fk.plan_total_blocks(segs) == len(S)
 
 
+def test_plan_batch_records_map_back_to_their_requests():
+    """A batch record carries `first` in place of its request's index; the
+    header's rule recovers the index -- the last r with offsets[r] <= first
+    -- and it is the oracle's request index for every record, with empty
+    requests (equal offsets) in the batch, including at its ends.  Each
+    record's blocks then sit inside its request's lists."""
+    g = np.random.default_rng(17)
+    for trial in range(20):
+        sizes = [int(x) for x in g.integers(0, 12, size=int(g.integers(1, 9)))]
+        if trial % 4 == 0:
+            sizes = [0] + sizes + [0, 0]
+        tables = []
+        for i, n in enumerate(sizes):
+            # a few sender runs of random length, a shuffled receiver side
+            S = np.sort(g.choice(60, size=n, replace=False)).astype(np.int32)
+            D = (1000 * i + np.sort(g.choice(200, size=n, replace=False))).astype(np.int32)
+            tables.append((S, D))
+        off = np.concatenate(([0], np.cumsum(sizes))).astype(np.int64)
+        S_all = np.concatenate([t[0] for t in tables]) if sum(sizes) else np.zeros(0, np.int32)
+        D_all = np.concatenate([t[1] for t in tables]) if sum(sizes) else np.zeros(0, np.int32)
+        segs = fk.flowkv_plan_batch(off, S_all, D_all, 60, 1000 * len(sizes) + 200)
+        ref = oracle.plan_batch_ref([(a.tolist(), b.tolist()) for a, b in tables])
+        req = np.searchsorted(off, segs["first"], side="right") - 1
+        assert req.tolist() == [r[3] for r in ref]
+        for sg, r in zip(segs, req):
+            lo = int(sg["first"]) - int(off[r])
+            m = int(sg["n_blocks"])
+            assert 0 <= lo and lo + m <= sizes[r]
+            assert (tables[r][0][lo:lo + m] == sg["src_block"] + np.arange(m)).all()
+            assert (tables[r][1][lo:lo + m] == sg["dst_block"] + np.arange(m)).all()
+
+
 def test_plan_contiguous_is_one_and_stride2_is_n():
     n = 813
     segs = fk.flowkv_plan(np.arange(n), np.arange(100, 100 + n), 1000, 1000)
@@ -441,10 +473,15 @@ def test_plan_errors():
         fk.flowkv_plan_batch([0, 1, 2], [1, 2], [5, 5], P, P)
     assert e.value.code == fk.EDUP
     assert len(fk.flowkv_plan_batch([0, 1, 2], [1, 1], [5, 6], P, P)) == 2
-    for off in ([1, 2], [0, 2, 1]):
+    for off in ([1, 2], [0, 3, 2]):             # not from 0, not non-decreasing
         with pytest.raises(fk.FlowKVError) as e:
             fk.flowkv_plan_batch(off, [1, 2], [3, 4], P, P)
         assert e.value.code == fk.EINVAL
+    # offsets that end past or short of the lists, or are not one row, never
+    # reach the planner (it would read past the lists or drop their tail)
+    for off in ([0, 5], [0, 1], [0, 2, 3], [], [[0, 2]]):
+        with pytest.raises(ValueError):
+            fk.flowkv_plan_batch(off, [1, 2], [3, 4], P, P)
     assert len(fk.flowkv_plan([], [], P, P)) == 0
 
 
@@ -593,7 +630,8 @@ def test_transfer_request_rejects_before_any_device_call():
     assert req(bm, bm2, [1000], [0])[0] == fk.ERANGE
     assert req(bm, bm2, [1, 1], [2, 3])[0] == fk.EDUP
     assert req(bm, bm2, [], []) == (fk.OK, 0)
-    assert req(bm, bm, [], [])[0] == fk.EINVAL                      # overlapping pools
+    assert req(bm, bm, [], []) == (fk.EINVAL, -1)                   # overlapping pools
+    assert req(bm, bm, [0, 1], [5, 6]) == (fk.EINVAL, -1)           # n_runs left untouched
     stride2 = 2 * np.arange(301)
     assert req(bm, bm2, stride2, stride2 + 1) == (fk.ECAP, 301)      # block-major: 300 fit
     assert req(bm, lm, np.arange(65) * 2, np.arange(65) * 2) == (fk.ECAP, 65)   # else 64
@@ -645,3 +683,4 @@ def test_attention_rejects_bad_arguments_without_touching_the_device():
     assert attn(pool(L=2, B=8, chunk=chunk + 16)) == fk.EINVAL    # chunk not bs x Hkv x Dh x 2
     assert attn(pool(layout=7, L=2, B=8, chunk=chunk)) == fk.EINVAL
     assert attn(pool(L=2, B=8, chunk=chunk, bases=(0,))) == fk.EINVAL   # NULL base
+
