@@ -127,13 +127,41 @@ def moved_blocks_equal(src: fk.KVPool, dst: fk.KVPool, S, D) -> bool:
     return True
 
 
+def block_checksums(pool: fk.KVPool, piece_bytes: int = 256 << 20) -> torch.Tensor:
+    """Two checksums of every block of a device pool, computed on the device
+    with torch: the sum of the block's 32-bit words, and the sum of each word
+    times a weight that depends on its position in the block (1 .. 4093), both
+    in int64 (no overflow for blocks under 2 GiB).  Returns (num_blocks, 2)
+    int64 on the device.  A write into a block changes them unless it
+    happens to preserve both sums."""
+    B, dev = pool.num_blocks, pool.device
+    out = torch.zeros((B, 2), dtype=torch.int64, device=dev)
+    if pool.layout == BM:
+        parts = [(pool.tensors[0].view(torch.int32).reshape(B, -1), 0)]
+    else:   # chunk (layer l, K/V kv) of every block, at word offset (2 l + kv) x chunk words
+        cw = pool.chunk_bytes // 4
+        parts = [(t[kv].view(torch.int32).reshape(B, -1), (2 * l + kv) * cw)
+                 for l, t in enumerate(pool.tensors) for kv in range(2)]
+    for words, base in parts:
+        w = ((torch.arange(words.shape[1], device=dev, dtype=torch.int64) + base) % 4093) + 1
+        step = max(1, piece_bytes // (4 * words.shape[1]))
+        for lo in range(0, B, step):
+            x = words[lo:lo + step].to(torch.int64)
+            out[lo:lo + step, 0] += x.sum(1)
+            out[lo:lo + step, 1] += (x * w).sum(1)
+            del x
+    return out
+
+
 def check_sampled(wl, wl_ref, sl, dl, max_blocks=1536, untouched_frac=0.01, max_untouched=1024,
                   seed_sample=7, inline=False, **cfg):
     """Full-size comparison: a seeded sample of the moved blocks (all of them
     when there are at most max_blocks) against the oracle; every moved block
-    against its sender block on the device (`moved_blocks_equal`); and the
-    guard blocks around every receiver run plus a seeded sample of the other
-    receiver blocks against their pre-image.
+    against its sender block on the device (`moved_blocks_equal`); the guard
+    blocks around every receiver run plus a seeded sample of the other
+    receiver blocks against their pre-image, byte for byte; and every other
+    receiver block of the whole pool against its pre-image by the two
+    checksums of `block_checksums`.
 
     `wl` holds the block lists from the library's allocator (they drive the
     device path), `wl_ref` the same workload from the oracle's allocator
@@ -166,7 +194,14 @@ def check_sampled(wl, wl_ref, sl, dl, max_blocks=1536, untouched_frac=0.01, max_
     rest = rest[sample_indices(rest.size, k, seed_sample + 1)] if k else rest[:0]
     keep = np.unique(np.concatenate((guards[:max_untouched], rest))).astype(np.int64)
     before = download_blocks(dst, keep)
+    sums_before = block_checksums(dst)
     run_transfer(src, dst, segs, inline=inline, **cfg)
+    untouched = torch.as_tensor(~touched, device=dst.device)
+    sums_after = block_checksums(dst)
+    changed = (sums_after != sums_before).any(1) & untouched
+    assert not bool(changed.any()), \
+        f"untouched receiver blocks changed: {torch.nonzero(changed)[:8].flatten().tolist()}"
+    del sums_before, sums_after, untouched, changed
     # oracle on compact pools: sampled logical block i moves from compact
     # sender block i to compact receiver block i
     expect = oracle.HostPool.zeros(dl, geom.num_layers, len(pick), geom.block_size,

@@ -277,7 +277,8 @@ def build(recipe, *args):
 
 
 @pytest.mark.parametrize("policy", ["fifo_sorted", "segment"])
-@pytest.mark.parametrize("sl,dl", [(BM, BM), (LM, LM), (LM, BM)], ids=lambda x: NAMES[x])
+@pytest.mark.parametrize("sl,dl", [(BM, BM), (LM, LM), (LM, BM), (BM, LM)],
+                         ids=lambda x: NAMES[x])
 def test_llama8b_13k_full_size(policy, sl, dl):
     wl, ref = build(recipes.llama8b_13k, policy)
     say(f"8b 13k {policy} {NAMES[sl]}->{NAMES[dl]}: {wl.n_blocks} blocks")
@@ -311,7 +312,8 @@ def test_batch32_full_size(policy, sl, dl):
     say(f"  {len(segs)} runs, {nb} blocks checked")
 
 
-@pytest.mark.parametrize("policy,sl,dl", [("segment", BM, BM), ("fifo_shuffled", LM, LM)])
+@pytest.mark.parametrize("policy,sl,dl", [("segment", BM, BM), ("fifo_shuffled", LM, LM),
+                                          ("segment", BM, LM)])
 def test_llama70b_tp8_full_size(policy, sl, dl):
     wl, ref = build(recipes.llama70b_tp8, policy)
     say(f"70b tp8 {policy} {NAMES[sl]}->{NAMES[dl]}: {wl.n_blocks} blocks")
