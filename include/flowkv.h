@@ -31,7 +31,9 @@
  *     planners and *n_runs of flowkv_transfer_request on FLOWKV_ECAP.
  *   - The caller owns every buffer.  The library allocates no device memory and
  *     keeps no pointer after a call returns, except inside an allocator or a
- *     scheduler handle.
+ *     scheduler handle, and except the fixed scratch array of
+ *     flowkv_decode_attention_noalloc (a static device array of the library's
+ *     code object, not an allocation).
  *   - Block IDs and counts are int32; byte sizes and offsets are 64-bit.
  *   - Allocator and scheduler handles are not thread-safe; planners, the
  *     transfer and attention are reentrant.
@@ -338,6 +340,33 @@ int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer, const void* 
                             int32_t max_seq_len, float scale, int32_t split_tokens,
                             float* out_dev, void* workspace_dev, int64_t workspace_bytes,
                             void* hip_stream);
+
+/* For callers that cannot allocate device memory or pass a workspace: code
+   under HIP graph capture, serving loops and harnesses that forbid
+   hipMalloc.  flowkv_decode_attention with the workspace replaced by
+   FLOWKV_ATTN_SCRATCH_BYTES of device memory the library holds on each GPU it
+   runs on, from the first call on that GPU until the process ends.  The call
+   allocates nothing (no hipMalloc, hipFree or allocating library routine);
+   the first call on a GPU looks up that GPU's copy of the array
+   (hipGetSymbolAddress) with the GPU current.  The caller still passes q,
+   the block tables, the lengths and the output, as for
+   flowkv_decode_attention, with the same results for the same inputs.
+   ECAP, with nothing launched, when the call needs more partial results
+   than the scratch holds: flowkv_decode_attention_workspace(...) above
+   FLOWKV_ATTN_SCRATCH_BYTES (16 MiB covers, for example, 32 requests of up
+   to 20,480 tokens with 32 query heads of head_dim 128 at the default
+   split).  Calls on one GPU share its scratch: calls that overlap on that
+   GPU (other streams, other threads) race and give undefined results;
+   serialise them.  Other arguments and errors as for
+   flowkv_decode_attention. */
+#define FLOWKV_ATTN_SCRATCH_BYTES 16777216 /* 16 MiB */
+
+int flowkv_decode_attention_noalloc(const flowkv_pool* pool, int32_t layer, const void* q_dev,
+                                    int32_t n_req, int32_t q_heads, int32_t kv_heads,
+                                    int32_t head_dim, const int32_t* block_tables_dev,
+                                    int32_t max_blocks, const int32_t* seq_lens_dev,
+                                    int32_t max_seq_len, float scale, int32_t split_tokens,
+                                    float* out_dev, void* hip_stream);
 
 /* ---- load-aware scheduler (section 3.4; Appendix A, Algorithm 1) ------------
    Host only.  Each node reports a status vector S_i of 12 indicators, in

@@ -44,8 +44,10 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #include "flowkv.h"
 #include "flowkv_status.h"
@@ -836,6 +838,21 @@ extern "C" int flowkv_decode_attention_workspace(int32_t n_req, int32_t q_heads,
   return ok();
 }
 
+namespace {
+
+// Checks every argument, then enqueues both passes with `ws` (ws_cap bytes)
+// as the workspace.  When `scratch_ws` is set, the workspace is the library's
+// own device array (found after the checks, so a call rejected on its
+// arguments makes no runtime call) and a short capacity is reported as such.
+int launch_attention(const flowkv_pool* pool, int32_t layer, const void* q_dev, int32_t n_req,
+                     int32_t q_heads, int32_t kv_heads, int32_t head_dim,
+                     const int32_t* block_tables_dev, int32_t max_blocks,
+                     const int32_t* seq_lens_dev, int32_t max_seq_len, float scale,
+                     int32_t split_tokens, float* out_dev, void* ws, int64_t ws_cap,
+                     bool scratch_ws, void* hip_stream);
+
+}  // namespace
+
 extern "C" int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer,
                                        const void* q_dev, int32_t n_req, int32_t q_heads,
                                        int32_t kv_heads, int32_t head_dim,
@@ -844,6 +861,81 @@ extern "C" int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer,
                                        float scale, int32_t split_tokens, float* out_dev,
                                        void* workspace_dev, int64_t workspace_bytes,
                                        void* hip_stream) {
+  return launch_attention(pool, layer, q_dev, n_req, q_heads, kv_heads, head_dim,
+                          block_tables_dev, max_blocks, seq_lens_dev, max_seq_len, scale,
+                          split_tokens, out_dev, workspace_dev, workspace_bytes, false,
+                          hip_stream);
+}
+
+// ---- the variant that allocates nothing --------------------------------------
+//
+// Its partial results live in `scratch`, a file-scope device array: each GPU
+// the library runs on holds its own copy for the life of the process.  In
+// host code `scratch` names a host-side stand-in, not device memory; the
+// device address of the current GPU's copy comes from hipGetSymbolAddress,
+// looked up once per device on its first call and kept in g_scratch_addr.
+// Nothing in the array needs to start at zero: pass 1 writes every split
+// record the merge reads.  Calls that overlap on one GPU share the array and
+// race.
+static __device__ __align__(256) float scratch[FLOWKV_ATTN_SCRATCH_BYTES / sizeof(float)];
+static_assert(FLOWKV_ATTN_SCRATCH_BYTES % 256 == 0, "scratch size in whole 256-byte units");
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+
+std::atomic<void*> g_scratch_addr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of the current GPU's copy of `scratch`.
+int scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(FLOWKV_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(FLOWKV_EINVAL, "device %d: the scratch table holds devices 0..%d", dev,
+                kMaxDevices - 1);
+  void* p = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_addr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !p)
+        return fail(FLOWKV_EHIP, "scratch address on device %d: %s", dev,
+                    hipGetErrorString(e));
+      g_scratch_addr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return FLOWKV_OK;
+}
+
+}  // namespace
+
+extern "C" int flowkv_decode_attention_noalloc(const flowkv_pool* pool, int32_t layer,
+                                               const void* q_dev, int32_t n_req,
+                                               int32_t q_heads, int32_t kv_heads,
+                                               int32_t head_dim,
+                                               const int32_t* block_tables_dev,
+                                               int32_t max_blocks, const int32_t* seq_lens_dev,
+                                               int32_t max_seq_len, float scale,
+                                               int32_t split_tokens, float* out_dev,
+                                               void* hip_stream) {
+  return launch_attention(pool, layer, q_dev, n_req, q_heads, kv_heads, head_dim,
+                          block_tables_dev, max_blocks, seq_lens_dev, max_seq_len, scale,
+                          split_tokens, out_dev, nullptr, FLOWKV_ATTN_SCRATCH_BYTES, true,
+                          hip_stream);
+}
+
+namespace {
+
+int launch_attention(const flowkv_pool* pool, int32_t layer, const void* q_dev, int32_t n_req,
+                     int32_t q_heads, int32_t kv_heads, int32_t head_dim,
+                     const int32_t* block_tables_dev, int32_t max_blocks,
+                     const int32_t* seq_lens_dev, int32_t max_seq_len, float scale,
+                     int32_t split_tokens, float* out_dev, void* workspace_dev,
+                     int64_t workspace_bytes, bool scratch_ws, void* hip_stream) {
   if (!pool) return fail(FLOWKV_EINVAL, "NULL pool");
   if (pool->layout != FLOWKV_LAYOUT_LAYER_MAJOR && pool->layout != FLOWKV_LAYOUT_BLOCK_MAJOR)
     return fail(FLOWKV_EINVAL, "unknown layout %d", pool->layout);
@@ -885,11 +977,18 @@ extern "C" int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer,
   if (n_req == 0) return ok();
   const int64_t need = ws_bytes(n_req, q_heads, head_dim, max_seq_len, split_tokens);
   // (a workspace of 0 bytes, when max_seq_len is 0, may be NULL)
-  if (!q_dev || !block_tables_dev || !seq_lens_dev || !out_dev || (!workspace_dev && need > 0))
+  if (!q_dev || !block_tables_dev || !seq_lens_dev || !out_dev ||
+      (!scratch_ws && !workspace_dev && need > 0))
     return fail(FLOWKV_EINVAL, "NULL device pointer");
-  if (workspace_bytes < need)
+  if (workspace_bytes < need) {
+    if (scratch_ws)
+      return fail(FLOWKV_ECAP,
+                  "%lld bytes of partial results needed, the library's scratch holds %lld "
+                  "(fewer requests or query heads per call, or a longer split)",
+                  (long long)need, (long long)workspace_bytes);
     return fail(FLOWKV_ECAP, "workspace of %lld bytes, %lld needed", (long long)workspace_bytes,
                 (long long)need);
+  }
   if (reinterpret_cast<uintptr_t>(q_dev) % 16)
     return fail(FLOWKV_EINVAL, "query not 16-byte aligned");
   // the launch grids put requests and splits on dimensions limited to 65,535
@@ -904,6 +1003,10 @@ extern "C" int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer,
     if (!pool->layer_base[i] || reinterpret_cast<uintptr_t>(pool->layer_base[i]) % 16)
       return fail(FLOWKV_EINVAL, "pool base pointer %d NULL or not 16-byte aligned", i);
     a.base[i] = static_cast<const char*>(pool->layer_base[i]);
+  }
+  if (scratch_ws && need > 0) {
+    const int rc = scratch_address(&workspace_dev);
+    if (rc) return rc;
   }
   a.pool_blocks = pool->num_blocks;
   a.chunk_bytes = pool->chunk_bytes;
@@ -942,3 +1045,5 @@ extern "C" int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer,
   if (e != hipSuccess) return fail(FLOWKV_EHIP, "attention launch: %s", hipGetErrorString(e));
   return ok();
 }
+
+}  // namespace

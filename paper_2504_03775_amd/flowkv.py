@@ -121,6 +121,13 @@ SIGNATURES = {
                                                ctypes.c_void_p, ctypes.c_int32, ctypes.c_float,
                                                ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                                ctypes.c_int64, ctypes.c_void_p]),
+    "flowkv_decode_attention_noalloc": (ctypes.c_int, [_POOLP, ctypes.c_int32, ctypes.c_void_p,
+                                                       ctypes.c_int32, ctypes.c_int32,
+                                                       ctypes.c_int32, ctypes.c_int32,
+                                                       ctypes.c_void_p, ctypes.c_int32,
+                                                       ctypes.c_void_p, ctypes.c_int32,
+                                                       ctypes.c_float, ctypes.c_int32,
+                                                       ctypes.c_void_p, ctypes.c_void_p]),
     "flowkv_sched_create": (ctypes.c_int, [ctypes.POINTER(flowkv_sched_params), ctypes.c_int32,
                                            ctypes.c_void_p, ctypes.POINTER(ctypes.c_void_p)]),
     "flowkv_sched_destroy": (None, [ctypes.c_void_p]),
@@ -541,6 +548,9 @@ def flowkv_decode_attention_workspace(n_req: int, q_heads: int, head_dim: int,
     return b.value
 
 
+ATTN_SCRATCH_BYTES = 16 << 20  # scratch of flowkv_decode_attention_noalloc, per GPU
+
+
 def _check_attention_tensors(pool: KVPool, q, block_tables, seq_lens, out):
     import torch
 
@@ -552,6 +562,21 @@ def _check_attention_tensors(pool: KVPool, q, block_tables, seq_lens, out):
     if tuple(out.shape) != (n, hq, dh) or block_tables.shape[0] != n or seq_lens.shape[0] != n:
         raise ValueError("attention tensors: shapes disagree")
     return n, hq, dh
+
+
+def flowkv_decode_attention_noalloc(pool: KVPool, layer: int, q, block_tables, seq_lens,
+                                    max_seq_len: int, scale: float, out,
+                                    split_tokens: int = 0, stream=None) -> None:
+    """flowkv_decode_attention without a workspace argument: the partial
+    results go to the library's fixed per-GPU scratch (ATTN_SCRATCH_BYTES);
+    calls that overlap on one GPU race."""
+    n, hq, dh = _check_attention_tensors(pool, q, block_tables, seq_lens, out)
+    _check(_lib.flowkv_decode_attention_noalloc(
+        ctypes.byref(pool.desc), layer, ctypes.c_void_p(q.data_ptr()), n, hq, pool.kv_heads, dh,
+        ctypes.c_void_p(block_tables.data_ptr()), block_tables.shape[1],
+        ctypes.c_void_p(seq_lens.data_ptr()), max_seq_len, scale, split_tokens,
+        ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(_stream_handle(stream))),
+        "flowkv_decode_attention_noalloc")
 
 
 def flowkv_decode_attention(pool: KVPool, layer: int, q, block_tables, seq_lens,

@@ -41,6 +41,7 @@ def test_binding_constants_match_the_header():
     defines = dict(re.findall(r"#define\s+(FLOWKV_\w+)\s+(-?\d+)", text))
     assert int(defines["FLOWKV_INLINE_RUNS"]) == fk.INLINE_RUNS
     assert int(defines["FLOWKV_INLINE_RUNS_BLOCK_MAJOR"]) == fk.INLINE_RUNS_BLOCK_MAJOR
+    assert int(defines["FLOWKV_ATTN_SCRATCH_BYTES"]) == fk.ATTN_SCRATCH_BYTES
     enums = dict(re.findall(r"\b(FLOWKV_E?\w+)\s*=\s*(-?\d+)", text))
     for name in ("OK", "EINVAL", "ENOSPC", "ERANGE", "EDUP", "ECAP", "EHIP", "ENOMEM"):
         assert int(enums["FLOWKV_" + name]) == getattr(fk, name), name
@@ -684,3 +685,34 @@ def test_attention_rejects_bad_arguments_without_touching_the_device():
     assert attn(pool(layout=7, L=2, B=8, chunk=chunk)) == fk.EINVAL
     assert attn(pool(L=2, B=8, chunk=chunk, bases=(0,))) == fk.EINVAL   # NULL base
 
+
+def attn_noalloc(p, layer=0, q=1 << 12, n_req=1, hq=8, hkv=2, dh=128, tables=1 << 16,
+                 max_blocks=4, lens=1 << 18, max_seq=64, scale=0.1, split=0, out=1 << 20):
+    return fk.lib().flowkv_decode_attention_noalloc(
+        ctypes.byref(p), layer, ctypes.c_void_p(q), n_req, hq, hkv, dh, ctypes.c_void_p(tables),
+        max_blocks, ctypes.c_void_p(lens), max_seq, scale, split, ctypes.c_void_p(out), None)
+
+
+def test_noalloc_attention_rejects_before_any_runtime_call():
+    """The allocation-free variant checks its arguments as the workspace form
+    does, and rejects a call whose partial results exceed the library's
+    scratch (ECAP) before it looks the scratch up: on this host, with no GPU,
+    every one of these returns without a runtime call."""
+    chunk = 16 * 2 * 128 * 2
+    p = pool(L=2, B=8, chunk=chunk)
+    assert fk.ATTN_SCRATCH_BYTES == 16 << 20
+    assert attn_noalloc(p, n_req=0) == fk.OK
+    for c in (dict(layer=2), dict(dh=96), dict(hq=6, hkv=4), dict(split=1025), dict(scale=0.0),
+              dict(q=(1 << 12) + 8), dict(q=0), dict(out=0), dict(max_blocks=-1)):
+        assert attn_noalloc(p, **c) == fk.EINVAL, c
+    # the need is n_req x q_heads x splits x (head_dim + 2) floats: find the
+    # largest request count that fits the scratch at 32 query heads over 8
+    # KV heads and 20,000 tokens, then one more
+    p8 = pool(L=2, B=8, chunk=16 * 8 * 128 * 2)
+    per_req = fk.flowkv_decode_attention_workspace(1, 32, 128, 20000, 1024)
+    fits = fk.ATTN_SCRATCH_BYTES // per_req
+    assert fk.flowkv_decode_attention_workspace(fits + 1, 32, 128, 20000, 1024) \
+        > fk.ATTN_SCRATCH_BYTES
+    rc = attn_noalloc(p8, n_req=fits + 1, hq=32, hkv=8, max_seq=20000, split=1024)
+    assert rc == fk.ECAP
+    assert "scratch holds 16777216" in fk.lib().flowkv_last_error().decode()
