@@ -476,6 +476,23 @@ def bench_schedule(args):
                           if k_ in ("requests_per_s", "ttft_mean_s", "e2e_mean_s",
                                     "role_switches", "scenario_ticks")}
         sim[name] = row
+    # the extreme scenarios' scaling (low load read as the lower thresholds
+    # eps_min = 0.05): a busy phase then a quiet one, 2 prefill + 2 decode
+    # nodes and 2 offline spares, against four fixed nodes
+    from workloads.cluster_sim import DECODE, OFFLINE, PREFILL
+    phased = Workload(0.5, 300, [1000, 4000, 8000], [128, 512], seed=4,
+                      phases=((20.0, 12.0), (60.0, 0.5)))
+    row = {}
+    for label, r6, scaling in (("four_fixed_nodes", [PREFILL, PREFILL, DECODE, DECODE], False),
+                               ("scaling_with_spares", [PREFILL, PREFILL, DECODE, DECODE,
+                                                        OFFLINE, OFFLINE], True)):
+        c = Cluster(ClusterConfig(roles=r6, scaling=scaling),
+                    NativeScheduler(fk, fk.sched_params(4, *pargs[1:], 0.05, 0.05), r6))
+        out = c.run(phased)
+        row[label] = {k_: (round(v, 4) if isinstance(v, float) else v) for k_, v in out.items()
+                      if k_ in ("requests_per_s", "ttft_mean_s", "e2e_mean_s", "node_seconds",
+                                "scale_requests", "scale_downs", "scenario_ticks")}
+    sim["busy-then-quiet"] = row
     line = {
         "metric": "load-aware scheduler evaluations per second (1,024 nodes, window 8)",
         "value": round(1.0 / t_eval, 1), "unit": "evaluations/s", "n_gpus": 1,

@@ -381,8 +381,11 @@ int flowkv_decode_attention_noalloc(const flowkv_pool* pool, int32_t layer, cons
        C_i^d = w_d . (L_r^d, L_w^d, L_sw^d, L_se^d, T_b, KV_u, G_u, MB_u)
    (term by term in that order), averages C_i^p over the prefill-role nodes
    and C_i^d over the decode-role nodes (0 for a role with no node), and
-   picks the scenario: normal when |C^p| <= eps_p_low and |C^d| <= eps_d_low;
-   imbalanced when both are within the high thresholds; extreme otherwise.
+   picks the scenario, testing in this order: low load when |C^p| < eps_p_min
+   and |C^d| < eps_d_min; normal when |C^p| <= eps_p_low and |C^d| <=
+   eps_d_low; imbalanced when both are within the high thresholds; extreme
+   (overload) otherwise.  Offline nodes (FLOWKV_ROLE_OFFLINE) report status
+   but count in no average, no idle set and no route.
    Readings of what Algorithm 1 leaves open:
      - idle nodes (imbalanced) are the nodes of the less loaded role whose
        own-role score is below idle_threshold; they are to take the busier
@@ -391,6 +394,12 @@ int flowkv_decode_attention_noalloc(const flowkv_pool* pool, int32_t layer, cons
        its high threshold once the scenario has lasted scale_after
        consecutive evaluations (the count restarts after each scale request
        and after any other scenario);
+     - low load is the other extreme scenario section 3.4 names (Appendix
+       A: scale up or, conversely, down once the scores have lasted);
+       Algorithm 1's branches would read it as normal, so it is tested
+       first, against a lower pair of thresholds (0 = never).  Once it has
+       lasted scale_after consecutive evaluations, each role with more than
+       one node may give one up (scale_* = -1), with its own count;
      - routing (flowkv_sched_route) takes the prefill node with the least
        (queued tokens + prompt tokens not in its prefix cache) / prefill
        rate, then the decode node with room for the KV bytes and the least
@@ -403,11 +412,12 @@ int flowkv_decode_attention_noalloc(const flowkv_pool* pool, int32_t layer, cons
 #define FLOWKV_SCHED_TERMS 8
 #define FLOWKV_SCHED_MAX_WINDOW 4096
 
-enum { FLOWKV_ROLE_PREFILL = 0, FLOWKV_ROLE_DECODE = 1 };
+enum { FLOWKV_ROLE_PREFILL = 0, FLOWKV_ROLE_DECODE = 1, FLOWKV_ROLE_OFFLINE = 2 };
 enum {
   FLOWKV_SCENARIO_NORMAL = 0,
   FLOWKV_SCENARIO_IMBALANCED = 1,
-  FLOWKV_SCENARIO_EXTREME = 2
+  FLOWKV_SCENARIO_EXTREME = 2,  /* overload */
+  FLOWKV_SCENARIO_LOW_LOAD = 3  /* the extreme scenario's low-load side */
 };
 
 typedef struct flowkv_sched_params {
@@ -419,14 +429,16 @@ typedef struct flowkv_sched_params {
   double eps_p_low, eps_d_low;            /* > 0 */
   double eps_p_high, eps_d_high;          /* >= the low thresholds */
   double idle_threshold;
+  double eps_p_min, eps_d_min;            /* low load below both; 0 <= min <= low */
 } flowkv_sched_params;
 
 typedef struct flowkv_sched_result {
   int32_t scenario;       /* FLOWKV_SCENARIO_* */
   int32_t n_idle;         /* idle node indices written (imbalanced), else 0 */
   int32_t switch_to;      /* the role idle nodes take (imbalanced), else -1 */
-  int32_t scale_prefill;  /* 1: add a prefill node (extreme, persisted) */
-  int32_t scale_decode;   /* 1: add a decode node */
+  int32_t scale_prefill;  /* +1: add a prefill node (overload, persisted);
+                             -1: one may go offline (low load, persisted) */
+  int32_t scale_decode;   /* the same for the decode role */
   int32_t reserved;
   double c_prefill;       /* C^p */
   double c_decode;        /* C^d */
@@ -435,13 +447,14 @@ typedef struct flowkv_sched_result {
 typedef struct flowkv_sched flowkv_sched; /* opaque, host memory only */
 
 /* New scheduler for n_nodes nodes (1..2^20) with initial roles[n_nodes]
-   (FLOWKV_ROLE_*).  The parameters are copied.  EINVAL for bad parameters,
+   (FLOWKV_ROLE_*, offline included).  The parameters are copied.  EINVAL for bad parameters,
    ENOSPC if host memory runs out. */
 int flowkv_sched_create(const flowkv_sched_params* params, int32_t n_nodes,
                         const int32_t* roles, flowkv_sched** out);
 void flowkv_sched_destroy(flowkv_sched* s);
 
-/* Change one node's role (a hybrid node switching, or a new node's role). */
+/* Change one node's role (a hybrid node switching, a node going offline
+   after a scale-down, or an offline node joining after a scale-up). */
 int flowkv_sched_set_role(flowkv_sched* s, int32_t node, int32_t role);
 
 /* One sample of every node's status: status[n_nodes x 12], row-major. */

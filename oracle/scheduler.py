@@ -7,15 +7,23 @@ and a decode score C_i^d as weighted sums, averages them over the prefill and
 the decode nodes (C^p, C^d) and compares the averages with thresholds to
 pick the scenario:
 
-    normal      |C^p| <= eps_p_low  and |C^d| <= eps_d_low
+    low load    |C^p| <  eps_p_min  and |C^d| <  eps_d_min    (an extreme case)
+    normal      |C^p| <= eps_p_low  and |C^d| <= eps_d_low    (otherwise)
     imbalanced  |C^p| <= eps_p_high and |C^d| <= eps_d_high   (otherwise)
-    extreme     anything else
+    extreme     anything else (overload)
 
 Normal load routes a request to the prefill node with the smallest
 time-to-first-token given its prefix-cache hit, then to the decode node with
 the smallest transfer latency from that prefill node.  Imbalanced load names
 the idle nodes (score below a threshold) so their hybrid schedulers take the
-busier role.  Extreme load that lasts asks for more nodes.
+busier role.  Extreme load that lasts asks for more nodes (overload) or for
+fewer (low load).  Section 3.4 counts both system overload and low load as
+extreme scenarios, and Appendix A's extreme-load paragraph scales up or,
+conversely, down once the scores have lasted; Algorithm 1's own branches
+test only the upper thresholds, under which low load would read as normal.
+The reading here adds the lower pair (eps_p_min, eps_d_min), tested first;
+0 turns it off.  Nodes may also be offline (a third role): they report
+status but take part in no average, no idle set and no route.
 
 The paper leaves the window, the normalisation, the weights, the thresholds,
 the TTFT and latency models and the role an idle node takes unstated; this
@@ -39,11 +47,15 @@ Parity: the steps Algorithm 1 states are pinned in
 - averages over own-role nodes only;
 - hand-worked scenario boundaries, idle sets and the persistence of
   extreme load;
-- routing against brute force over every (prefill, decode) pair.
+- routing against brute force over every (prefill, decode) pair;
+- low load: strict lower thresholds tested first, its own persistence count,
+  scale-down only for roles with more than one node, offline nodes in no
+  average, idle set or route, all worked by hand.
 
 The readings themselves (window, normalisation, weights, thresholds, the
-TTFT and latency models, the idle node's new role) are **parity unpinned**:
-the paper prints no example or number to check them against.
+TTFT and latency models, the idle node's new role, the low-load thresholds
+and the scale-down rule) are **parity unpinned**: the paper prints no example
+or number to check them against.
 """
 
 from __future__ import annotations
@@ -52,8 +64,8 @@ from dataclasses import dataclass, field
 from typing import List, Sequence, Tuple
 
 N_IND = 12
-PREFILL, DECODE = 0, 1
-NORMAL, IMBALANCED, EXTREME = 0, 1, 2
+PREFILL, DECODE, OFFLINE = 0, 1, 2
+NORMAL, IMBALANCED, EXTREME, LOW_LOAD = 0, 1, 2, 3
 
 # the indicators each role's score reads, in the order of its weights
 TERMS = {PREFILL: (0, 1, 2, 3, 8, 9, 10, 11), DECODE: (4, 5, 6, 7, 8, 9, 10, 11)}
@@ -71,6 +83,8 @@ class Params:
     eps_d_high: float
     idle_threshold: float
     scale_after: int                # consecutive extreme evaluations before scaling
+    eps_p_min: float = 0.0          # low load: both averages below these (0: never)
+    eps_d_min: float = 0.0
 
 
 @dataclass
@@ -80,8 +94,8 @@ class Result:
     c_decode: float
     idle: List[int] = field(default_factory=list)
     switch_to: int = -1             # role the idle nodes take (imbalanced), else -1
-    scale_prefill: int = 0          # 1: the prefill side asks for another node
-    scale_decode: int = 0
+    scale_prefill: int = 0          # +1: the prefill side asks for another node,
+    scale_decode: int = 0           # -1: it can give one up (low load)
 
 
 class RefScheduler:
@@ -94,15 +108,18 @@ class RefScheduler:
             raise ValueError("bad weights or scale_after")
         if not (0 < p.eps_p_low <= p.eps_p_high and 0 < p.eps_d_low <= p.eps_d_high):
             raise ValueError("thresholds need 0 < low <= high")
-        if any(r not in (PREFILL, DECODE) for r in roles) or not roles:
-            raise ValueError("roles must be PREFILL or DECODE")
+        if not (0 <= p.eps_p_min <= p.eps_p_low and 0 <= p.eps_d_min <= p.eps_d_low):
+            raise ValueError("low-load thresholds need 0 <= min <= low")
+        if any(r not in (PREFILL, DECODE, OFFLINE) for r in roles) or not roles:
+            raise ValueError("roles must be PREFILL, DECODE or OFFLINE")
         self.p = p
         self.roles = list(roles)
         self.history: List[List[List[float]]] = [[] for _ in roles]  # per node: samples
-        self.extreme_run = 0
+        self.extreme_run = 0        # consecutive overload evaluations
+        self.low_run = 0            # consecutive low-load evaluations
 
     def set_role(self, node: int, role: int) -> None:
-        if role not in (PREFILL, DECODE):
+        if role not in (PREFILL, DECODE, OFFLINE):
             raise ValueError("bad role")
         self.roles[node] = role
 
@@ -154,11 +171,25 @@ class RefScheduler:
             if role == PREFILL:
                 sp += scores[i][0]
                 n += 1
-            else:
+            elif role == DECODE:
                 sd += scores[i][1]
                 m += 1
         cp = sp / n if n else 0.0
         cd = sd / m if m else 0.0
+        # Reading: low load -- both averages under their lower thresholds --
+        # is the extreme scenario's other side; once it has lasted
+        # scale_after evaluations each role with more than one node may give
+        # one up
+        if abs(cp) < p.eps_p_min and abs(cd) < p.eps_d_min:
+            self.extreme_run = 0
+            self.low_run += 1
+            r = Result(LOW_LOAD, cp, cd)
+            if self.low_run >= p.scale_after:
+                r.scale_prefill = -int(n > 1)
+                r.scale_decode = -int(m > 1)
+                self.low_run = 0
+            return r
+        self.low_run = 0
         if abs(cp) <= p.eps_p_low and abs(cd) <= p.eps_d_low:
             self.extreme_run = 0
             return Result(NORMAL, cp, cd)
@@ -170,7 +201,7 @@ class RefScheduler:
             # relative to its low threshold)
             busier = PREFILL if cp / p.eps_p_low >= cd / p.eps_d_low else DECODE
             idle = [i for i, role in enumerate(self.roles)
-                    if role != busier and scores[i][role] < p.idle_threshold]
+                    if role not in (busier, OFFLINE) and scores[i][role] < p.idle_threshold]
             return Result(IMBALANCED, cp, cd, idle, busier)
         # Reading: extreme load asks for another node of each side beyond its
         # high threshold once the scenario has lasted scale_after evaluations

@@ -21,7 +21,9 @@ constexpr int kTerms = FLOWKV_SCHED_TERMS;
 constexpr int kPrefillTerms[kTerms] = {0, 1, 2, 3, 8, 9, 10, 11};
 constexpr int kDecodeTerms[kTerms] = {4, 5, 6, 7, 8, 9, 10, 11};
 
-bool valid_role(int32_t r) { return r == FLOWKV_ROLE_PREFILL || r == FLOWKV_ROLE_DECODE; }
+bool valid_role(int32_t r) {
+  return r == FLOWKV_ROLE_PREFILL || r == FLOWKV_ROLE_DECODE || r == FLOWKV_ROLE_OFFLINE;
+}
 
 }  // namespace
 
@@ -33,7 +35,8 @@ struct flowkv_sched {
   // sits at `head`, and `count` samples are valid (the same for every node)
   std::vector<double> ring;
   int32_t head = 0, count = 0;
-  int32_t extreme_run = 0;
+  int32_t extreme_run = 0;     // consecutive overload evaluations
+  int32_t low_run = 0;         // consecutive low-load evaluations
   std::vector<double> scores;  // scratch: (C_i^p, C_i^d) per node
 };
 
@@ -57,6 +60,9 @@ extern "C" int flowkv_sched_create(const flowkv_sched_params* params, int32_t n_
       !std::isfinite(p.eps_p_high) || !std::isfinite(p.eps_d_high) ||
       std::isnan(p.idle_threshold))
     return fail(FLOWKV_EINVAL, "thresholds need 0 < low <= high, finite");
+  if (!(p.eps_p_min >= 0 && p.eps_p_min <= p.eps_p_low && p.eps_d_min >= 0 &&
+        p.eps_d_min <= p.eps_d_low))
+    return fail(FLOWKV_EINVAL, "low-load thresholds need 0 <= min <= low");
   for (int32_t i = 0; i < n_nodes; ++i)
     if (!valid_role(roles[i])) return fail(FLOWKV_EINVAL, "role of node %d is %d", i, roles[i]);
   flowkv_sched* s = new (std::nothrow) flowkv_sched;
@@ -130,7 +136,7 @@ extern "C" int flowkv_sched_evaluate(flowkv_sched* s, flowkv_sched_result* res,
     if (s->roles[i] == FLOWKV_ROLE_PREFILL) {
       sp += s->scores[2 * size_t(i)];
       ++np;
-    } else {
+    } else if (s->roles[i] == FLOWKV_ROLE_DECODE) {
       sd += s->scores[2 * size_t(i) + 1];
       ++nd;
     }
@@ -140,25 +146,39 @@ extern "C" int flowkv_sched_evaluate(flowkv_sched* s, flowkv_sched_result* res,
   r.c_decode = nd ? sd / double(nd) : 0.0;
   r.switch_to = -1;
   int32_t n_idle = 0;
-  if (std::fabs(r.c_prefill) <= p.eps_p_low && std::fabs(r.c_decode) <= p.eps_d_low) {
+  if (std::fabs(r.c_prefill) < p.eps_p_min && std::fabs(r.c_decode) < p.eps_d_min) {
+    // low load: the extreme scenario's other side; once it has lasted, each
+    // role with more than one node may give one up
+    r.scenario = FLOWKV_SCENARIO_LOW_LOAD;
+    s->extreme_run = 0;
+    if (++s->low_run >= p.scale_after) {
+      r.scale_prefill = np > 1 ? -1 : 0;
+      r.scale_decode = nd > 1 ? -1 : 0;
+      s->low_run = 0;
+    }
+  } else if (std::fabs(r.c_prefill) <= p.eps_p_low && std::fabs(r.c_decode) <= p.eps_d_low) {
     r.scenario = FLOWKV_SCENARIO_NORMAL;
     s->extreme_run = 0;
+    s->low_run = 0;
   } else if (std::fabs(r.c_prefill) <= p.eps_p_high && std::fabs(r.c_decode) <= p.eps_d_high) {
     r.scenario = FLOWKV_SCENARIO_IMBALANCED;
     s->extreme_run = 0;
+    s->low_run = 0;
     const int32_t busier = r.c_prefill / p.eps_p_low >= r.c_decode / p.eps_d_low
                                ? FLOWKV_ROLE_PREFILL
                                : FLOWKV_ROLE_DECODE;
     r.switch_to = busier;
     for (int32_t i = 0; i < s->n; ++i) {
       const int32_t role = s->roles[i];
-      if (role != busier && s->scores[2 * size_t(i) + role] < p.idle_threshold) {
+      if (role != busier && role != FLOWKV_ROLE_OFFLINE &&
+          s->scores[2 * size_t(i) + role] < p.idle_threshold) {
         if (idle_nodes) idle_nodes[n_idle] = i;
         ++n_idle;
       }
     }
   } else {
     r.scenario = FLOWKV_SCENARIO_EXTREME;
+    s->low_run = 0;
     if (++s->extreme_run >= p.scale_after) {
       r.scale_prefill = std::fabs(r.c_prefill) > p.eps_p_high;
       r.scale_decode = std::fabs(r.c_decode) > p.eps_d_high;

@@ -64,7 +64,8 @@ class flowkv_sched_params(ctypes.Structure):
                 ("scale", ctypes.c_double * 12), ("w_prefill", ctypes.c_double * 8),
                 ("w_decode", ctypes.c_double * 8), ("eps_p_low", ctypes.c_double),
                 ("eps_d_low", ctypes.c_double), ("eps_p_high", ctypes.c_double),
-                ("eps_d_high", ctypes.c_double), ("idle_threshold", ctypes.c_double)]
+                ("eps_d_high", ctypes.c_double), ("idle_threshold", ctypes.c_double),
+                ("eps_p_min", ctypes.c_double), ("eps_d_min", ctypes.c_double)]
 
 
 class flowkv_sched_result(ctypes.Structure):
@@ -286,14 +287,15 @@ class Allocator:
 
 # ---- load-aware scheduler ------------------------------------------------------
 
-ROLE_PREFILL, ROLE_DECODE = 0, 1
-SCENARIO_NORMAL, SCENARIO_IMBALANCED, SCENARIO_EXTREME = 0, 1, 2
+ROLE_PREFILL, ROLE_DECODE, ROLE_OFFLINE = 0, 1, 2
+SCENARIO_NORMAL, SCENARIO_IMBALANCED, SCENARIO_EXTREME, SCENARIO_LOW_LOAD = 0, 1, 2, 3
 SCHED_INDICATORS = 12
 
 
 def sched_params(window: int, scale, w_prefill, w_decode, eps_p_low: float, eps_d_low: float,
                  eps_p_high: float, eps_d_high: float, idle_threshold: float,
-                 scale_after: int) -> flowkv_sched_params:
+                 scale_after: int, eps_p_min: float = 0.0,
+                 eps_d_min: float = 0.0) -> flowkv_sched_params:
     p = flowkv_sched_params()
     p.window, p.scale_after = window, scale_after
     p.scale[:] = [float(x) for x in scale]
@@ -302,6 +304,7 @@ def sched_params(window: int, scale, w_prefill, w_decode, eps_p_low: float, eps_
     p.eps_p_low, p.eps_d_low = eps_p_low, eps_d_low
     p.eps_p_high, p.eps_d_high = eps_p_high, eps_d_high
     p.idle_threshold = idle_threshold
+    p.eps_p_min, p.eps_d_min = eps_p_min, eps_d_min
     return p
 
 

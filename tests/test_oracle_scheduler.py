@@ -13,6 +13,10 @@ what the algorithm fixes whatever the unstated constants are:
 * imbalanced load: the idle set and the role it takes, worked by hand;
 * extreme load: the scale request arrives on exactly the scale_after-th
   consecutive evaluation and the count restarts after normal load;
+* low load (the reading that gives section 3.4's low-load extreme a branch):
+  strict lower thresholds tested before normal load, its own persistence
+  count, a scale-down only for roles with more than one node, and offline
+  nodes left out of averages, idle sets and routes, worked by hand;
 * routing: brute force over every (P, D) pair ordered by (TTFT, index),
   then (latency, index), on random small clusters; closed cases for full
   prefix hits and for no decode node with room.
@@ -23,8 +27,8 @@ import random
 
 import pytest
 
-from oracle.scheduler import (DECODE, EXTREME, IMBALANCED, NORMAL, PREFILL, Params,
-                              RefScheduler, default_params, route)
+from oracle.scheduler import (DECODE, EXTREME, IMBALANCED, LOW_LOAD, NORMAL, OFFLINE, PREFILL,
+                              Params, RefScheduler, default_params, route)
 
 ONE = [1.0] * 12
 
@@ -145,6 +149,67 @@ def test_extreme_scales_after_persisting():
                    (E, 0, 0), (E, 0, 0), (E, 1, 0)]
 
 
+@pytest.mark.parametrize("cp,cd,want", [
+    (0.2499999, 0.2499999, LOW_LOAD),   # both under the lower thresholds
+    (0.25, 0.0, NORMAL),                # strict: at the threshold is normal
+    (0.0, -0.25, NORMAL),               # |C|
+    (-0.1, 0.1, LOW_LOAD),
+    (0.0, 1.5, IMBALANCED),             # one side low, the other busy: not low load
+])
+def test_low_load_boundaries(cp, cd, want):
+    w = [1.0] + [0.0] * 7
+    wd = [0.0, 0.0, 0.0, 0.0, 1.0, 0.0, 0.0, 0.0]   # C^d = T_b
+    s = RefScheduler(params(w_prefill=w, w_decode=wd, eps_p_min=0.25, eps_d_min=0.25),
+                     [PREFILL, DECODE])
+    s.observe([[cp] + [0.0] * 11, [0.0] * 8 + [cd, 0.0, 0.0, 0.0]])
+    assert s.evaluate().scenario == want
+
+
+def test_low_load_is_off_at_zero_thresholds():
+    s = RefScheduler(params(), [PREFILL, DECODE])
+    s.observe([[0.0] * 12, [0.0] * 12])
+    assert s.evaluate().scenario == NORMAL
+
+
+def test_low_load_scales_down_after_persisting():
+    """Two prefill nodes and one decode node, all quiet: on the third
+    consecutive low-load evaluation the prefill side may give a node up; the
+    decode side, with its only node, may not.  Normal load restarts the
+    count; an overload run in between does not share it."""
+    w = [1.0] + [0.0] * 7
+    s = RefScheduler(params(w_prefill=w, scale_after=3, eps_p_min=0.5, eps_d_min=0.5),
+                     [PREFILL, PREFILL, DECODE])
+    quiet = [[0.0] * 12] * 3
+    mid = [[0.75] + [0.0] * 11, [0.75] + [0.0] * 11, [0.0] * 12]    # C^p 0.75: normal
+    hot = [[5.0] + [0.0] * 11, [5.0] + [0.0] * 11, [0.0] * 12]      # overload
+    got = []
+    for st in [quiet, quiet, quiet, quiet, mid, quiet, quiet, hot, quiet, quiet, quiet]:
+        s.observe(st)
+        r = s.evaluate()
+        got.append((r.scenario, r.scale_prefill, r.scale_decode))
+    L, N, E = LOW_LOAD, NORMAL, EXTREME
+    assert got == [(L, 0, 0), (L, 0, 0), (L, -1, 0), (L, 0, 0), (N, 0, 0),
+                   (L, 0, 0), (L, 0, 0), (E, 0, 0), (L, 0, 0), (L, 0, 0), (L, -1, 0)]
+
+
+def test_offline_nodes_take_no_part():
+    """An offline node's status counts in no average: with the busy node
+    offline the averages are those of the others; it is never idle and never
+    routed to."""
+    w = [1.0] + [0.0] * 7
+    wd = [0.0] * 4 + [1.0] + [0.0] * 3
+    s = RefScheduler(params(w_prefill=w, w_decode=wd), [PREFILL, OFFLINE, DECODE])
+    s.observe([[1.5] + [0.0] * 11, [9.0] * 12, [0.0] * 8 + [0.125, 0, 0, 0]])
+    r = s.evaluate()
+    assert (r.c_prefill, r.c_decode) == (1.5, 0.125)
+    assert r.scenario == IMBALANCED and r.switch_to == PREFILL and r.idle == [2]
+    roles = [PREFILL, OFFLINE, DECODE, OFFLINE]
+    z = [[0.0] * 4] * 4
+    assert route(roles, 100, [0] * 4, [0, 0, 0, 0], [1.0, 9.0, 1.0, 9.0], 1, z, z,
+                 [9, 9, 9, 9]) == (0, 2)
+    assert route([OFFLINE, DECODE], 100, [0, 0], [0, 0], [1.0, 1.0], 1, z, z, [9, 9]) == (-1, -1)
+
+
 def brute_route(roles, prompt, hit, queued, rate, kv, spb, lat, free):
     """Every (P, D) pair, ordered by (TTFT of P, P) then (latency P->D, D)."""
     P = [i for i, r in enumerate(roles) if r == PREFILL and rate[i] > 0]
@@ -201,7 +266,11 @@ def test_rejects_bad_parameters():
     with pytest.raises(ValueError):
         RefScheduler(params(scale=[1.0] * 11 + [0.0]), [PREFILL])
     with pytest.raises(ValueError):
-        RefScheduler(params(), [2])
+        RefScheduler(params(), [3])                       # no such role (2 is offline)
+    with pytest.raises(ValueError):
+        RefScheduler(params(eps_p_min=1.5), [PREFILL])    # low-load threshold above low
+    with pytest.raises(ValueError):
+        RefScheduler(params(eps_d_min=-0.5), [PREFILL])
     s = RefScheduler(default_params(), [PREFILL, DECODE])
     with pytest.raises(ValueError):
         s.evaluate()                                      # nothing observed yet

@@ -26,8 +26,14 @@ Model (all times in seconds):
   (queue lengths, token budget, KV and GPU use over the last tick) and
   evaluates.  Under imbalanced load the idle nodes it names switch to the
   busier role once they hold no work of their old role (a role keeps at
-  least one node); extreme-load scale requests are counted (the model has
-  no spare nodes to add).
+  least one node).  Scale requests are counted; with ``scaling`` on, the
+  model also applies them: a scale-up brings the lowest-indexed offline node
+  online in the role asked for, and a scale-down takes the role's
+  highest-indexed node offline once it has drained (a role keeps at least
+  one node).  Offline nodes report zeros and take no requests; the model
+  reports the node-seconds spent online (the cost that scaling down saves).
+* arrivals may change rate over time (``phases``: consecutive (duration,
+  rate) pieces), so one run can pass from busy to quiet and back.
 """
 
 from __future__ import annotations
@@ -36,11 +42,11 @@ import heapq
 import math
 from collections import deque
 from dataclasses import dataclass, field
-from typing import Dict, List, Optional, Sequence
+from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
-PREFILL, DECODE = 0, 1
+PREFILL, DECODE, OFFLINE = 0, 1, 2
 KV_BYTES_PER_TOKEN_8B = 32 * 2 * 8 * 128 * 2   # Llama-3-8B, bf16: 128 KiB per token
 
 
@@ -58,6 +64,7 @@ class ClusterConfig:
     kv_bytes_per_token: int = KV_BYTES_PER_TOKEN_8B
     tick: float = 0.1                       # scheduler period
     switching: bool = True                  # apply idle-node role switches
+    scaling: bool = False                   # apply scale-up / scale-down requests
 
 
 @dataclass
@@ -67,6 +74,7 @@ class Workload:
     prompts: Sequence[int]                  # prompt lengths, drawn uniformly
     outputs: Sequence[int]                  # output lengths, drawn uniformly
     seed: int = 0
+    phases: Optional[Sequence[Tuple[float, float]]] = None  # (duration s, rate); then `rate`
 
 
 # placeholder normalisation for the model's indicators (Algorithm 1 order)
@@ -114,8 +122,10 @@ class Cluster:
         self.log: List[tuple] = []          # (time, kind, ...) decisions, for comparisons
         self.done: List[_Req] = []
         self.switches = 0
-        self.scale_requests = [0, 0]
-        self.scenarios = [0, 0, 0]
+        self.scale_requests = [0, 0]        # scale-ups asked: prefill, decode
+        self.scale_downs = [0, 0]           # scale-downs asked: prefill, decode
+        self.scenarios = [0, 0, 0, 0]       # normal, imbalanced, overload, low load
+        self.node_seconds = 0.0             # time online, summed over nodes
         lat = [[cfg.link_latency] * self.n for _ in range(self.n)]
         spb = [[1.0 / cfg.link_rate] * self.n for _ in range(self.n)]
         self.lat, self.spb = lat, spb
@@ -231,7 +241,9 @@ class Cluster:
             g = min(1.0, nd.busy_time / cfg.tick)
             nd.busy_time = 0.0
             s = [0.0] * 12
-            if nd.role == PREFILL:
+            if nd.role == OFFLINE:
+                pass                            # an offline node reports zeros
+            elif nd.role == PREFILL:
                 s[0] = 1.0 if nd.busy is not None else 0.0
                 s[1] = float(len(nd.queue))
                 s[3] = float(nd.sending)
@@ -249,13 +261,23 @@ class Cluster:
         return out
 
     def _tick(self) -> None:
+        self.node_seconds += self.cfg.tick * sum(1 for nd in self.nodes if nd.role != OFFLINE)
         self.sched.observe(self._status())
         r = self.sched.evaluate()
         scen, idle, switch_to, sp, sd = r
         self.scenarios[scen] += 1
-        self.scale_requests[0] += sp
-        self.scale_requests[1] += sd
+        for k, x in enumerate((sp, sd)):
+            if x > 0:
+                self.scale_requests[k] += x
+            elif x < 0:
+                self.scale_downs[k] -= x
         self.log.append((self.now, "eval", scen, tuple(idle), switch_to, sp, sd))
+        if self.cfg.scaling:
+            for role, x in ((PREFILL, sp), (DECODE, sd)):
+                if x > 0:
+                    self._scale_up(role)
+                elif x < 0:
+                    self._scale_down(role)
         if self.cfg.switching and idle:
             for i in idle:
                 nd = self.nodes[i]
@@ -269,6 +291,22 @@ class Cluster:
             self.backlog.popleft()
         if len(self.done) < self.total:
             self._at(self.now + self.cfg.tick, "tick")
+
+    def _scale_up(self, role: int) -> None:
+        for i, nd in enumerate(self.nodes):
+            if nd.role == OFFLINE and nd.pending is None:
+                nd.role = role
+                self.sched.set_role(i, role)
+                self.log.append((self.now, "online", i, role))
+                return
+
+    def _scale_down(self, role: int) -> None:
+        active = [i for i, nd in enumerate(self.nodes) if nd.role == role and nd.pending is None]
+        if len(active) > 1:
+            i = active[-1]
+            self.nodes[i].pending = OFFLINE
+            self.log.append((self.now, "retire", i))
+            self._maybe_switch(i)
 
     def _admit(self, req: _Req) -> bool:
         """Route a request; queue it at its prefill node if both sides exist."""
@@ -290,18 +328,27 @@ class Cluster:
         if drained:
             nd.role, nd.pending = nd.pending, None
             self.sched.set_role(i, nd.role)
-            self.switches += 1
-            self.log.append((self.now, "switch", i, nd.role))
+            if nd.role == OFFLINE:
+                self.log.append((self.now, "offline", i))
+            else:
+                self.switches += 1
+                self.log.append((self.now, "switch", i, nd.role))
 
     # ---- driver --------------------------------------------------------------
     def run(self, wl: Workload, horizon: float = 3600.0) -> Dict[str, float]:
         rng = np.random.default_rng(wl.seed)
-        gaps = rng.exponential(1.0 / wl.rate, wl.n_requests)
+        gaps = rng.exponential(1.0, wl.n_requests)      # unit-rate gaps, scaled below
         prompts = rng.choice(np.asarray(wl.prompts), wl.n_requests)
         outputs = rng.choice(np.asarray(wl.outputs), wl.n_requests)
+        # piecewise rates: phase j covers [ends[j-1], ends[j]); `rate` after
+        ends, rates = [], []
+        for dur, rate in (wl.phases or ()):
+            ends.append((ends[-1] if ends else 0.0) + dur)
+            rates.append(rate)
         t = 0.0
         for k in range(wl.n_requests):
-            t += float(gaps[k])
+            j = next((i for i, e in enumerate(ends) if t < e), None)
+            t += float(gaps[k] * (1.0 / (rates[j] if j is not None else wl.rate)))
             self._at(t, "arrival", _Req(k, t, int(prompts[k]), int(outputs[k])))
         self.total = wl.n_requests
         self.backlog: deque = deque()
@@ -343,6 +390,8 @@ class Cluster:
             "role_switches": self.switches,
             "scenario_ticks": list(self.scenarios),
             "scale_requests": list(self.scale_requests),
+            "scale_downs": list(self.scale_downs),
+            "node_seconds": round(self.node_seconds, 6),
         }
 
 
