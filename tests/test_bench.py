@@ -118,9 +118,12 @@ def test_schedule_line_contract_on_cpu():
     assert j["value"] > 0 and j["roofline"] is None and j["dtype"] == "f64"
     assert j["cpu_baseline"]["kind"] == "oracle" and j["cpu_baseline"]["value"] > 0
     sim = j["context"]["cluster_model_2p2d"]
-    assert set(sim) == {"balanced", "prefill-heavy", "decode-heavy"}
+    assert set(sim) == {"balanced", "prefill-heavy", "decode-heavy", "busy-then-quiet"}
     dh = sim["decode-heavy"]
     assert dh["load_aware"]["requests_per_s"] > dh["fixed"]["requests_per_s"]
+    bq = sim["busy-then-quiet"]
+    assert bq["scaling_with_spares"]["node_seconds"] < bq["four_fixed_nodes"]["node_seconds"]
+    assert bq["scaling_with_spares"]["scale_downs"][0] >= 1
 
 
 @pytest.mark.gpu
