@@ -100,6 +100,20 @@ __device__ __forceinline__ int clamp_len(const AttnArgs& a, int T) {
   return T < a.max_seq_len ? T : a.max_seq_len;
 }
 
+// A split at or past its request's end still leaves a record, an empty
+// partial (max -inf, sum 0) for each of its kG query heads, so that the merge
+// reads every split up to max_splits without the request's length.  Its
+// weighted-V part is never written; the merge ignores it.
+template <int kG, int kDh>
+__device__ __forceinline__ void write_empty_partial(const AttnArgs& a, int g, int split, int r,
+                                                    int tid) {
+  if (tid < kG) {
+    float* e = a.ws + ((int64_t(r) * a.q_heads + g * kG + tid) * a.max_splits + split) * (kDh + 2);
+    e[0] = -INFINITY;
+    e[1] = 0.f;
+  }
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
@@ -185,7 +199,10 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
       s_blk[i] = a.tables[int64_t(r) * a.max_blocks + b0 + i];
   }
   const int T = clamp_len(a, a.seq_lens[r]);
-  if (t0 >= T) return;  // uniform: this split is past the request's end
+  if (t0 >= T) {  // uniform: this split is past the request's end
+    write_empty_partial<kG, kDh>(a, g, split, r, tid);
+    return;
+  }
   const int t1 = t0 + a.split_tokens < T ? t0 + a.split_tokens : T;
 
   // this lane's query pairs for each of the row's heads (raw bf16)
@@ -479,7 +496,10 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split_mfma(const AttnArg
       s_blk[i] = a.tables[int64_t(r) * a.max_blocks + b0 + i];
   }
   const int T = clamp_len(a, a.seq_lens[r]);
-  if (t0 >= T) return;  // uniform: this split is past the request's end
+  if (t0 >= T) {  // uniform: this split is past the request's end
+    write_empty_partial<kG, kDh>(a, g, split, r, tid);
+    return;
+  }
   const int t1 = t0 + a.split_tokens < T ? t0 + a.split_tokens : T;
 
   // Q as the A operand of q.k: Q[head c16][32 i + 8 q4 .. + 8]; rows past G are zero
@@ -726,58 +746,76 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split_mfma(const AttnArg
   }
 }
 
-// Pass 2: one workgroup per (query head, request).  The largest split
-// reference comes first (all threads over the splits, then across the
-// workgroup); then 256 / Dh thread sets each take every (256 / Dh)-th split,
-// eight splits' loads in flight per thread, and the sets' sums meet in LDS.
+// Pass 2: one workgroup per (query head, request).  Every split up to
+// max_splits has a record (pass 1 leaves an empty one past a request's end),
+// so the merge needs no request length and no chain of dependent loads: a
+// thread set of Dh threads takes every (256 / Dh)-th split, kMergeChunk
+// splits' records loaded at once (all of them in one round for up to
+// 256 / Dh x kMergeChunk splits), folded into a running (max, sum, weighted V)
+// that is rescaled when its max rises; the sets then meet in LDS.
 constexpr int kMergeThreads = 256;
+constexpr int kMergeChunk = 16;
 
 template <int kDh>
 __global__ __launch_bounds__(kMergeThreads) void decode_attn_merge(const AttnArgs a) {
   constexpr int kParts = kMergeThreads / kDh;
   const int h = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
   const int d = tid % kDh, part = tid / kDh;
-  const int T = clamp_len(a, a.seq_lens[r]);
+  const int ns = a.max_splits;
   float* o = a.out + (int64_t(r) * a.q_heads + h) * kDh;
-  if (T <= 0) {
-    if (part == 0) o[d] = 0.f;
-    return;
-  }
-  const int ns = (T + a.split_tokens - 1) / a.split_tokens;
-  const float* src = a.ws + (int64_t(r) * a.q_heads + h) * a.max_splits * (kDh + 2);
-
-  __shared__ float s_red[kMergeThreads / 64];
-  float M = -INFINITY;
-  for (int x = tid; x < ns; x += kMergeThreads) M = fmaxf(M, src[int64_t(x) * (kDh + 2)]);
+  const float* src = a.ws + (int64_t(r) * a.q_heads + h) * ns * (kDh + 2);
+  float m = -INFINITY, l = 0.f, acc = 0.f;
+  for (int x0 = part; x0 < ns; x0 += kParts * kMergeChunk) {
+    // branch-free loads: a split past the end re-reads split 0 and is
+    // masked; an empty record's weighted V (never written) is not used
+    float ms[kMergeChunk], ls[kMergeChunk], vs[kMergeChunk];
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
-  if (tid % 64 == 0) s_red[tid / 64] = M;
-  __syncthreads();
+    for (int j = 0; j < kMergeChunk; ++j) {
+      const int x = x0 + j * kParts;
+      const float* e = src + int64_t(x < ns ? x : 0) * (kDh + 2);
+      ms[j] = e[0];
+      ls[j] = e[1];
+      vs[j] = e[2 + d];
+      if (x >= ns) ms[j] = -INFINITY;
+    }
+    // no branch on the records' values, so every load above issues at once
+    float cm = m;
 #pragma unroll
-  for (int w = 0; w < kMergeThreads / 64; ++w) M = fmaxf(M, s_red[w]);
-
-  float L = 0.f, A = 0.f;
-#pragma unroll 8
-  for (int x = part; x < ns; x += kParts) {
-    const float* e = src + int64_t(x) * (kDh + 2);
-    const float ms = e[0];
-    const float w = ms == -INFINITY ? 0.f : exp2f(ms - M);
-    L = fmaf(e[1], w, L);
-    A = fmaf(e[2 + d], w, A);
+    for (int j = 0; j < kMergeChunk; ++j) cm = fmaxf(cm, ms[j]);
+    const float c = m == -INFINITY ? 0.f : exp2f(m - cm);  // 1 when the max holds
+    l *= c;
+    acc *= c;
+#pragma unroll
+    for (int j = 0; j < kMergeChunk; ++j) {
+      const bool live = ms[j] != -INFINITY;
+      const float w = live ? exp2f(ms[j] - cm) : 0.f;
+      l = live ? fmaf(ls[j], w, l) : l;
+      acc = live ? fmaf(vs[j], w, acc) : acc;
+    }
+    m = cm;
   }
+  __shared__ float s_m[kParts], s_l[kParts];
   __shared__ float s_a[kParts][kDh];
-  __shared__ float s_l[kParts];
-  s_a[part][d] = A;
-  if (d == 0) s_l[part] = L;
+  if (d == 0) {
+    s_m[part] = m;
+    s_l[part] = l;
+  }
+  s_a[part][d] = acc;
   __syncthreads();
   if (part == 0) {
-    float At = 0.f, Lt = 0.f;
+    float M = -INFINITY;
+#pragma unroll
+    for (int p = 0; p < kParts; ++p) M = fmaxf(M, s_m[p]);
+    float L = 0.f, A = 0.f;
 #pragma unroll
     for (int p = 0; p < kParts; ++p) {
-      At += s_a[p][d];
-      Lt += s_l[p];
+      if (s_m[p] != -INFINITY) {
+        const float w = exp2f(s_m[p] - M);
+        L = fmaf(s_l[p], w, L);
+        A = fmaf(s_a[p][d], w, A);
+      }
     }
-    o[d] = Lt > 0.f ? At / Lt : 0.f;
+    o[d] = L > 0.f ? A / L : 0.f;
   }
 }
 
