@@ -138,7 +138,7 @@ typedef struct flowkv_pool {
 } flowkv_pool;
 
 /* Optional launch shape for flowkv_transfer_ex; a zero field takes the
-   library's choice.
+   library's choice (order: 4 between two block-major pools, else 2).
    threads: workgroup size, a multiple of 64 in 64..1024.
    unroll:  16-byte vectors each thread moves per tile: 2, 4, 8 or 16.
    grid:    workgroups to launch, >= 1 (capped at the number of tiles).
@@ -146,7 +146,9 @@ typedef struct flowkv_pool {
             3 = nontemporal stores, 4 = nontemporal loads and stores.
    order:   the order workgroups visit tiles in: 1 = plan order, 2 = blocks
             scattered by a fixed permutation (a block's tiles stay together),
-            3 = tiles scattered by a fixed permutation.  Same result for all. */
+            3 = tiles scattered by a fixed permutation, 4 = tile-major: tile 0
+            of every block (blocks scattered as in 2), then tile 1, and so on.
+            Same result for all. */
 typedef struct flowkv_launch_config {
   int32_t threads;
   int32_t unroll;

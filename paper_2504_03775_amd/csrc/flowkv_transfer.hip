@@ -13,7 +13,9 @@
 // default one tile per workgroup).  By default the blocks are visited in a
 // fixed scattered order (x -> x * m mod total_blocks), so the workgroups
 // resident at one moment spread over the whole plan instead of streaming
-// one window of neighbouring tiles.  A workgroup finds the run holding
+// one window of neighbouring tiles; between two block-major pools the
+// tiles go tile-major (tile 0 of every block in that order, then tile 1, and
+// so on).  A workgroup finds the run holding
 // its tile by a galloping search over the runs' `first` fields, starting
 // where equal-length runs would put it: O(log distance) per jump, nothing
 // while it stays inside a run.
@@ -69,7 +71,8 @@ struct XferShape {
   int32_t tiles_per_block;  // ceil(lines_per_block / unroll)
   uint32_t h_magic;         // division by H (per-lane path)
   uint32_t h_shift;
-  int32_t order;            // 1 plan order, 2 blocks scattered, 3 tiles scattered
+  int32_t order;            // 1 plan order, 2 blocks scattered, 3 tiles scattered,
+                            // 4 tile-major over scattered blocks
   int64_t perm_mul;         // multiplier of the scattering permutation
 };
 
@@ -353,7 +356,8 @@ __global__ __launch_bounds__(1024) void kv_segment_copy(const A a) {
   flowkv_segment seg{};
   for (; u < a.units; u += stride) {
     // the tile this iteration visits: plan order, or a fixed permutation of
-    // blocks (2) or tiles (3) that scatters neighbouring workgroups
+    // blocks (2) or tiles (3) that scatters neighbouring workgroups, or tile
+    // by tile over scattered blocks (4)
     int64_t g = gl;
     int32_t t = tl;
     if (a.order == 2) {
@@ -362,6 +366,11 @@ __global__ __launch_bounds__(1024) void kv_segment_copy(const A a) {
       const int64_t v = u * a.perm_mul % a.units;
       g = v / a.tiles_per_block;
       t = int32_t(v - g * a.tiles_per_block);
+    } else if (a.order == 4) {
+      // tile-major: tile 0 of every block (blocks scattered), then tile 1 ...
+      const int64_t tt = u / a.total_blocks;
+      g = (u - tt * a.total_blocks) * a.perm_mul % a.total_blocks;
+      t = int32_t(tt);
     }
     if (s < 0 || g < seg.first || g - seg.first >= int64_t(seg.n_blocks)) {
       s = find_run<kInline>(a, segs, a.n_segs, g, (s < 0 || a.order != 1) ? guess_run(a, g) : s);
@@ -469,15 +478,20 @@ bool contiguous_plan(const flowkv_segment* r, int64_t n, int64_t total_blocks) {
 
 // Library defaults, from interleaved launch-shape comparisons over the five
 // transfer workloads in both layouts: 1024 threads moving 4 vectors each per
-// tile (64 KiB tiles), nontemporal loads and stores, one tile per workgroup,
-// blocks visited in scattered order.  Scattering matters for block-major
-// pools holding long contiguous runs (the segment allocator's output): in
-// plan order the resident workgroups stream one contiguous window of each
-// pool, which ran 7-11% slower; for other plans it is neutral (within 1%).
+// tile (64 KiB tiles), nontemporal loads and stores, one tile per workgroup.
+// Visiting order: in plan order the resident workgroups of block-major pools
+// stream one contiguous window of each pool, which ran 7-11% slower on the
+// segment allocator's long runs.  Between two block-major pools the tiles are
+// visited tile-major over scattered blocks (the resident workgroups then
+// touch one 64 KiB piece each of many blocks): 0.3-1.2% faster than blocks
+// scattered whole, except 0.4% slower on the 70B share.  With a layer-major
+// pool on either side tile-major ran 13% slower, and blocks are scattered
+// whole (a block's tiles then already span every layer tensor).
 constexpr int kDefaultThreads = 1024;
 constexpr int kDefaultUnroll = 4;
-constexpr int kDefaultCache = 4;  // nontemporal loads and stores
-constexpr int kDefaultOrder = 2;  // blocks scattered
+constexpr int kDefaultCache = 4;    // nontemporal loads and stores
+constexpr int kDefaultOrder = 2;    // blocks scattered
+constexpr int kDefaultOrderBM = 4;  // both pools block-major: tile-major
 constexpr uint64_t kPermPrime = 2654435761ull;
 constexpr int64_t kMaxGridPerCU = 2048;
 
@@ -579,7 +593,9 @@ int launch_transfer(const flowkv_pool* src, const flowkv_pool* dst,
                 layer_begin, layer_count, src->num_layers);
 
   int threads = kDefaultThreads, unroll = kDefaultUnroll, cache = kDefaultCache, grid = 0;
-  int order = kDefaultOrder;
+  const bool both_bm =
+      src->layout == FLOWKV_LAYOUT_BLOCK_MAJOR && dst->layout == FLOWKV_LAYOUT_BLOCK_MAJOR;
+  int order = both_bm ? kDefaultOrderBM : kDefaultOrder;
   if (cfg) {
     if (cfg->threads) threads = cfg->threads;
     if (cfg->unroll) unroll = cfg->unroll;
@@ -587,7 +603,7 @@ int launch_transfer(const flowkv_pool* src, const flowkv_pool* dst,
     if (cfg->order) order = cfg->order;
     grid = cfg->grid;
   }
-  if (order < 1 || order > 3) return fail(FLOWKV_EINVAL, "order %d: need 1..3", order);
+  if (order < 1 || order > 4) return fail(FLOWKV_EINVAL, "order %d: need 1..4", order);
   if (threads < 64 || threads > 1024 || threads % 64)
     return fail(FLOWKV_EINVAL, "threads %d: need a multiple of 64 in 64..1024", threads);
   if (unroll != 2 && unroll != 4 && unroll != 8 && unroll != 16)
@@ -599,8 +615,6 @@ int launch_transfer(const flowkv_pool* src, const flowkv_pool* dst,
   // compact form: block-major pools on both sides, the planner's records
   bool compact = false;
   if (inl && n_segs > kInlineRuns) {
-    const bool both_bm = src->layout == FLOWKV_LAYOUT_BLOCK_MAJOR &&
-                         dst->layout == FLOWKV_LAYOUT_BLOCK_MAJOR;
     if (!both_bm || n_segs > kInlineRunsBM)
       return fail(FLOWKV_ECAP,
                   "%lld runs: at most %d travel in the kernel arguments (%d between "

@@ -559,7 +559,7 @@ def test_transfer_rejects_bad_pools_without_touching_the_device():
     # launch shapes outside the documented limits
     for cfg in (fk.flowkv_launch_config(96, 8, 0, 0), fk.flowkv_launch_config(2048, 8, 0, 0),
                 fk.flowkv_launch_config(256, 3, 0, 0), fk.flowkv_launch_config(256, 8, -1, 0),
-                fk.flowkv_launch_config(256, 8, 0, 9), fk.flowkv_launch_config(256, 8, 0, 0, 4),
+                fk.flowkv_launch_config(256, 8, 0, 9), fk.flowkv_launch_config(256, 8, 0, 0, 5),
                 fk.flowkv_launch_config(256, 8, 0, 0, -1)):
         assert xfer(good_src, good_dst, n_segs=0, total=0, cfg=cfg) == fk.EINVAL
     # layer ranges of the layer-wise entry point

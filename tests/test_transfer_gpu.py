@@ -59,7 +59,8 @@ CONFIGS = [dict(), dict(threads=64), dict(threads=128, unroll=2), dict(threads=5
            dict(threads=1024, unroll=4), dict(grid=1), dict(grid=3, unroll=2),
            dict(cache=1), dict(cache=2), dict(cache=3), dict(cache=4, unroll=16, grid=5),
            dict(order=2), dict(order=3), dict(order=2, grid=7, threads=256),
-           dict(order=3, grid=2, unroll=4), dict(order=1, grid=4)]
+           dict(order=3, grid=2, unroll=4), dict(order=1, grid=4), dict(order=4),
+           dict(order=4, grid=5, threads=256), dict(order=4, threads=128, unroll=2)]
 
 
 def random_case(seed):
