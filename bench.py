@@ -55,6 +55,14 @@ HBM_PEAK_GBPS = 8000.0
 METRIC = "effective KV transfer GB/s (% of HBM peak); ms per 13k-token request transfer"
 KERNEL_SRC = os.path.join(ROOT, "paper_2504_03775_amd", "csrc", "flowkv_transfer.hip")
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "kv_segment_copy_llama3-8b-13k_pmc.txt")
+# counter summaries per (workload, layout) of the transfer kernel
+PMC_SUMMARIES = {
+    ("8b", "block"): PMC_SUMMARY,
+    ("8b", "layer"): os.path.join(ROOT, "profiles",
+                                  "kv_segment_copy_llama3-8b-13k_layer-major_pmc.txt"),
+    ("70b-shuffled", "layer"): os.path.join(ROOT, "profiles",
+                                            "kv_segment_copy_70b-shuffled_layer-major_pmc.txt"),
+}
 ATTN_SRC = os.path.join(ROOT, "paper_2504_03775_amd", "csrc", "flowkv_attention.hip")
 
 # hipEventDisableSystemFence (hip_runtime_api.h): recording the event skips
@@ -156,14 +164,18 @@ def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1,
                     help="GPUs to use: 1 only (the path runs on one device)")
-    ap.add_argument("--op", choices=["transfer", "attention", "schedule", "overlap"],
+    ap.add_argument("--op", choices=["transfer", "attention", "schedule", "overlap", "table3"],
                     default="transfer",
                     help="transfer: the KV transfer hot path (default); attention: one decode "
                          "step of paged attention over the receiver pool of the batch workload; "
                          "schedule: the load-aware scheduler (host) at 1,024 nodes, and the "
                          "cluster model's three load mixes with fixed and load-aware roles; "
                          "overlap: the 13k request's transfer after, or layer by layer beside, "
-                         "a prefill stand-in")
+                         "a prefill stand-in; table3: one launch against 32 per-layer launches "
+                         "at Table 3's input lengths")
+    ap.add_argument("--lengths", default="",
+                    help="table3: comma-separated input lengths in tokens (default: Table 3's "
+                         "500, 1000, 2000, 4000, 8000, 10000, 12000)")
     ap.add_argument("--steps", type=int, default=100, help="timed steps")
     ap.add_argument("--warmup", type=int, default=10, help="untimed steps before them")
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="8b")
@@ -691,6 +703,140 @@ hipMemcpyDeviceToDeviceNoCU, one call per run, layer and K-or-V):
     print(json.dumps(line), flush=True)
 
 
+TABLE3_LENGTHS = [500, 1000, 2000, 4000, 8000, 10000, 12000]
+# Table 3's FlowKV and FlowKV-Layerwise transfer latencies in seconds, single
+# L20 server (NVIDIA, NCCL): context only, another machine and another link
+TABLE3_PAPER_S = {500: (0.0044, 0.0678), 1000: (0.0075, 0.1309), 2000: (0.0126, 0.2565),
+                  4000: (0.0236, 0.5338), 8000: (0.0447, 1.1173), 10000: (0.0555, 1.4121),
+                  12000: (0.0681, 1.7218)}
+
+
+def bench_table3(args):
+    """FlowKV vs FlowKV-Layerwise across input lengths (section 4.4, Table
+    3) on one MI355X: Llama-3-8B KV of one request of T tokens for each of
+    the table's lengths, moved between the bench's two 65,536-block pools
+    (sender blocks from the segment allocator, receiver blocks from the
+    seeded free list of the 30%-occupied pool), in two forms:
+      one_launch  the whole plan in one launch (plan in the kernel arguments
+                  when it fits there, else staged);
+      layerwise   32 launches, one per layer (K and V of that layer).
+    Per form and length: the median kernel time (HIP events around the
+    launches), the step time back to back, and the synchronised request
+    latency (plan, staging, launches and kernels, synchronised; median of
+    20).  `value` is the mean synchronised one-launch latency over the
+    lengths (the paper's column mean, 0.0309 s on one L20 server)."""
+    import numpy as np
+    import torch
+
+    from paper_2504_03775_amd import flowkv as fk
+    from workloads import make_device_pool, recipes
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    layout = fk.LAYOUT_BLOCK_MAJOR if args.layout == "block" else fk.LAYOUT_LAYER_MAJOR
+    lengths = [int(x) for x in args.lengths.split(",")] if args.lengths else TABLE3_LENGTHS
+    make_alloc = lambda P, pol, seed: fk.Allocator(P, pol, seed)  # noqa: E731
+    wl0 = recipes.llama8b_13k(make_alloc, args.dst_policy, tokens=max(lengths),
+                              occupied=args.dst_occupied)
+    geom = wl0.geom
+    src = fk.KVPool(layout, make_device_pool(geom, layout, wl0.src_pool_blocks, dev, seed=0))
+    dst = fk.KVPool(layout, make_device_pool(geom, layout, wl0.dst_pool_blocks, dev, seed=1))
+    stream = torch.cuda.current_stream()
+    stager = fk.PlanStager(dev, capacity=4096)
+    rows = []
+    gc.collect()
+    for T in lengths:
+        wl = recipes.llama8b_13k(make_alloc, args.dst_policy, tokens=T,
+                                 occupied=args.dst_occupied)
+        (S, D), = wl.tables
+        n = len(S)
+
+        def step(form, ev=None):
+            segs = fk.flowkv_plan(S, D, src.num_blocks, dst.num_blocks)
+            inline = form == "one_launch" and len(segs) <= fk.inline_capacity(src, dst)
+            segs_dev = None if inline else stager.stage(segs, stream)
+            if ev is not None:
+                ev[0].record(stream)
+            if inline:
+                fk.flowkv_transfer_inline(src, dst, segs, n, stream=stream)
+            elif form == "one_launch":
+                fk.flowkv_transfer_ex(src, dst, segs_dev, len(segs), n, stream=stream)
+            else:
+                for layer in range(geom.num_layers):
+                    fk.flowkv_transfer_layers(src, dst, segs_dev, len(segs), n, layer, 1,
+                                              stream=stream)
+            if ev is not None:
+                ev[1].record(stream)
+            if not inline:
+                stager.release(stream)
+            return len(segs)
+
+        row = {"tokens": T, "blocks": n, "payload_bytes": n * geom.block_bytes}
+        for form in ("one_launch", "layerwise"):
+            runs = step(form)
+            torch.cuda.synchronize()
+            i = n // 2
+            if layout == fk.LAYOUT_BLOCK_MAJOR:
+                assert torch.equal(src.tensors[0][int(S[i])], dst.tensors[0][int(D[i])])
+            for _ in range(args.warmup):
+                step(form)
+            evs = timing_pairs(args.steps)
+            torch.cuda.synchronize()
+            gc.disable()
+            t0 = time.perf_counter()
+            for e in evs:
+                step(form, e)
+            torch.cuda.synchronize()
+            el = time.perf_counter() - t0
+            lat = []
+            for _ in range(20):
+                torch.cuda.synchronize()
+                t1 = time.perf_counter()
+                step(form)
+                torch.cuda.synchronize()
+                lat.append((time.perf_counter() - t1) * 1e3)
+            gc.enable()
+            k_ms = statistics.median(a.elapsed_time(b) for a, b in evs)
+            row[form] = {"kernel_ms_median": round(k_ms, 4),
+                         "ms_per_step": round(el * 1e3 / args.steps, 4),
+                         "latency_ms_median": round(statistics.median(lat), 4),
+                         "launches": 1 if form == "one_launch" else geom.num_layers,
+                         "hbm_frac": round(2 * n * geom.block_bytes / (k_ms * 1e-3) / 1e9
+                                           / HBM_PEAK_GBPS, 4)}
+            row["runs"] = runs
+        row["layerwise_over_one_launch"] = {
+            k: round(row["layerwise"][k] / row["one_launch"][k], 2)
+            for k in ("kernel_ms_median", "ms_per_step", "latency_ms_median")}
+        if T in TABLE3_PAPER_S:
+            row["paper_s_single_l20"] = dict(zip(("flowkv", "flowkv_layerwise"),
+                                                 TABLE3_PAPER_S[T]))
+        rows.append(row)
+        print(f"table3 {T} tokens: one launch {row['one_launch']['latency_ms_median']} ms, "
+              f"per-layer {row['layerwise']['latency_ms_median']} ms", file=sys.stderr,
+              flush=True)
+    mean_lat = statistics.fmean(r["one_launch"]["latency_ms_median"] for r in rows)
+    line = {
+        "metric": "KV transfer latency per request, one launch (Table 3 FlowKV column, mean "
+                  "over input lengths)",
+        "value": round(mean_lat, 4), "unit": "ms", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(statistics.fmean(
+            r["one_launch"]["ms_per_step"] for r in rows), 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "u8",
+        "data": "synthetic",
+        "config": {"workload": "llama3-8b-kv-one-request-table3-lengths", "lengths": lengths,
+                   "layers": geom.num_layers, "kv_heads": geom.kv_heads,
+                   "head_dim": geom.head_dim, "block_size": geom.block_size,
+                   "kv_dtype": "bf16", "pool_blocks": [src.num_blocks, dst.num_blocks],
+                   "layout": f"{args.layout}-major", "receiver_policy": args.dst_policy,
+                   "receiver_occupied": args.dst_occupied},
+        "timing_events": TIMING["events"],
+        "rows": rows,
+        "roofline": None,
+        "cpu_baseline": None,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -705,6 +851,9 @@ def main():
         return
     if args.op == "overlap":
         bench_overlap(args)
+        return
+    if args.op == "table3":
+        bench_table3(args)
         return
 
     import numpy as np
@@ -988,6 +1137,26 @@ def main():
                 "roofline_frac": round((2 * payload + 16 * len(segs_alt)) / (k_alt * 1e-3) / 1e9
                                        / HBM_PEAK_GBPS, 4),
                 "ms_per_step": round(el_alt * 1e3 / args.steps, 4)}
+        # the same kernel on a plan of one run of the same bytes (sender
+        # blocks [0, n) to receiver blocks [0, n)): the copy's own ceiling
+        # for these pools, against which the plan's run structure is judged
+        if single and not args.calibration_only and not args.layerwise:
+            one = np.array([(0, 0, n, 0)], dtype=fk.SEGMENT_DTYPE)
+            for _ in range(args.warmup):
+                fk.flowkv_transfer_inline(src, dst, one, n, stream=stream, **cfg)
+            evs_one = timing_pairs(args.steps)
+            torch.cuda.synchronize()
+            for e in evs_one:
+                e[0].record(stream)
+                fk.flowkv_transfer_inline(src, dst, one, n, stream=stream, **cfg)
+                e[1].record(stream)
+            torch.cuda.synchronize()
+            k_one = statistics.fmean(a.elapsed_time(b) for a, b in evs_one)
+            context["single_run_plan"] = {
+                "runs": 1, "kernel_ms_avg": round(k_one, 4),
+                "roofline_frac": round((2 * payload + 16) / (k_one * 1e-3) / 1e9
+                                       / HBM_PEAK_GBPS, 4),
+                "note": "the same kernel, sender blocks [0, n) to receiver blocks [0, n)"}
 
     # ---- CPU baseline: the oracle on the host ----------------------------------------
     cpu = None
@@ -1039,8 +1208,9 @@ def main():
                                           f"threads, repeated {reps_m}x"}}
         del h_src, h_dst
 
-    traffic = traffic_from_profile(runs=n_runs) if (single and args.layout == "block"
-                                                   and not args.layerwise) else None
+    summary = PMC_SUMMARIES.get((args.workload, args.layout))
+    traffic = traffic_from_profile(summary, runs=n_runs) if summary and not args.layerwise \
+        else None
     kv_dtype = {"bfloat16": "bf16", "float16": "fp16"}[geom.dtype]
     config = {"workload": wl_desc, "layers": geom.num_layers, "kv_heads": geom.kv_heads,
               "head_dim": geom.head_dim, "block_size": geom.block_size, "kv_dtype": kv_dtype,
@@ -1069,8 +1239,13 @@ def main():
         "dtype": "u8",
         "data": "synthetic",
         "config": config,
+        "value_is": "payload bytes (each K/V byte moved counted once) per second of the "
+                    "timed back-to-back steps",
         ("ms_per_request" if single else "ms_per_plan_latency"): round(ms_latency, 4),
+        "hbm_gbps": round(achieved, 1),
         "pct_of_hbm_peak": round(100 * achieved / HBM_PEAK_GBPS, 2),
+        "hbm_is": "bytes read plus bytes written by the kernel per second of its own "
+                  "launches (HIP events)",
         "kernel_ms_avg": round(kern_avg_ms, 4),
         "kernel_ms_p10_p50_p90": [round(float(x), 4) for x in
                                   np.percentile(np.asarray(kern_ms), [10, 50, 90])],

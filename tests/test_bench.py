@@ -181,3 +181,26 @@ def test_overlap_line_contract():
     assert all(v > 0 for v in j["median_ms"].values())
     assert j["value"] == j["exposed_ms"]["layerwise_overlap"]
     assert j["config"]["tokens"] == 13000 and j["config"]["layers"] == 32
+
+
+@pytest.mark.gpu
+def test_table3_line_contract():
+    """bench.py --op table3: one launch and 32 per-layer launches at each
+    length asked for, each timed three ways, the ratio per length, and the
+    paper's two columns beside them as context."""
+    j = run_bench("--op", "table3", "--lengths", "500,4000", "--steps", "3", "--warmup", "1")
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
+                "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config",
+                "roofline", "cpu_baseline", "rows"):
+        assert key in j, key
+    assert j["unit"] == "ms" and j["higher_is_better"] is False and j["vs_baseline"] is None
+    assert [r["tokens"] for r in j["rows"]] == [500, 4000]
+    for r in j["rows"]:
+        assert r["blocks"] == -(-r["tokens"] // 16)
+        assert r["one_launch"]["launches"] == 1 and r["layerwise"]["launches"] == 32
+        for form in ("one_launch", "layerwise"):
+            assert all(r[form][k] > 0 for k in ("kernel_ms_median", "ms_per_step",
+                                                 "latency_ms_median"))
+        assert set(r["paper_s_single_l20"]) == {"flowkv", "flowkv_layerwise"}
+    assert j["value"] == pytest.approx(
+        sum(r["one_launch"]["latency_ms_median"] for r in j["rows"]) / 2, abs=1e-3)
