@@ -4,7 +4,9 @@ The oracle computes pool offsets with its own explicit formulas.  These tests
 read and write the pools only through numpy's shaped-array indexing of the
 Eq. 5 layouts -- (2, B, bs, slot) per layer for (L, 2, B, H), and
 (B, L, 2, bs, slot) for (B, L, 2, H) -- so a wrong stride, a swapped index or
-a dropped term in the oracle shows up as a wrong tag.
+a dropped term in the oracle shows up as a wrong tag.  The same views give the
+slot addresses that pin Eq. 5's point: a request's aligned runs are one
+contiguous copy each block-major and 2L each layer-major.
 """
 
 import itertools
@@ -251,3 +253,60 @@ def test_layer_by_layer_composes_to_the_whole_transfer(fn):
         assert np.array_equal(a, b)
     with pytest.raises(ValueError):
         fn(src, parts, S, D, layers=[L])
+
+
+# ---- Eq. 5's claim: the restructured layout cuts transfer operations by 2L ------
+
+def byte_address(pool: HostPool, b, l, kv, s):
+    """(buffer, byte offset) of one slot, read off numpy's shaped views."""
+    v = shaped(pool, np.uint8)
+    if pool.layout == LAYER_MAJOR:
+        buf, row = l, v[l][kv, b, s]
+    else:
+        buf, row = 0, v[b, l, kv, s]
+    return buf, row.ctypes.data - pool.buffers[buf].ctypes.data
+
+
+def contiguous_copies(src: HostPool, dst: HostPool, S, D) -> int:
+    """The fewest contiguous (sender range -> receiver range) copies that
+    perform the transfer's slot copies: the number of slot copies that no
+    other slot copy continues on both sides at once."""
+    sb = src.slot_bytes
+    copies = set()
+    for b_s, b_d in zip(S, D):
+        for l in range(src.num_layers):
+            for kv in (0, 1):
+                for s in range(src.block_size):
+                    copies.add(byte_address(src, int(b_s), l, kv, s) +
+                               byte_address(dst, int(b_d), l, kv, s))
+    return sum(1 for (i, o, j, p) in copies if (i, o - sb, j, p - sb) not in copies)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_block_major_needs_one_copy_per_run_layer_major_2L(seed):
+    """Section 3.3, Eq. 5: in the per-layer layout (L, 2, B, H) each aligned
+    run of blocks is 2L separate ranges (one per layer and K/V); in the
+    restructured layout (B, L, 2, H) it is one.  With ascending block lists
+    (as the allocators hand out) the fewest contiguous copies are exactly
+    the plan's runs block-major and 2L times as many layer-major; a fully
+    contiguous request is one copy."""
+    from oracle import plan_ref
+
+    g = np.random.default_rng(300 + seed)
+    L = int(g.integers(1, 4))
+    bs = int(g.choice([1, 2, 4]))
+    B = 40
+    n = int(g.integers(1, 14))
+    if seed % 6 == 0:                               # one contiguous run on both sides
+        s0, d0 = int(g.integers(1, B - n - 1)), int(g.integers(1, B - n - 1))
+        S, D = np.arange(s0, s0 + n), np.arange(d0, d0 + n)
+    else:                                           # ascending, gaps at random
+        S = np.sort(g.choice(np.arange(1, B - 1), n, replace=False))
+        D = np.sort(g.choice(np.arange(1, B - 1), n, replace=False))
+    runs = len(plan_ref(S.tolist(), D.tolist()))
+    if seed % 6 == 0:
+        assert runs == 1
+    for layout, per_run in ((BLOCK_MAJOR, 1), (LAYER_MAJOR, 2 * L)):
+        src = HostPool.zeros(layout, L, B, bs, 8)
+        dst = HostPool.zeros(layout, L, B, bs, 8)
+        assert contiguous_copies(src, dst, S, D) == per_run * runs, (layout, L, runs)
