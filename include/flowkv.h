@@ -94,6 +94,9 @@ enum {
 #define FLOWKV_INLINE_RUNS 64 /* plan records flowkv_transfer_inline carries */
 #define FLOWKV_INLINE_RUNS_BLOCK_MAJOR 300 /* ... between two block-major pools, as
                                               the planner writes them */
+#define FLOWKV_INLINE_LAYERS 32 /* pools of at most this many layers ...     */
+#define FLOWKV_INLINE_RUNS_LAYER_MAJOR 264 /* ... carry this many planner-form
+                                              records when either is layer-major */
 
 typedef struct flowkv_allocator flowkv_allocator; /* opaque, host memory only */
 
@@ -254,17 +257,30 @@ int flowkv_transfer_ex(const flowkv_pool* src, const flowkv_pool* dst,
    copied into the kernel's arguments at launch, so the plan needs no device
    buffer and no separate host-to-device copy; segs_host may be reused as
    soon as the call returns.  Same result as flowkv_transfer_ex with the same
-   plan in device memory.  Up to FLOWKV_INLINE_RUNS records fit; between two
-   block-major pools up to FLOWKV_INLINE_RUNS_BLOCK_MAJOR, provided the plan
-   is in the planner's form (record i starts where record i - 1 ends, every
-   record holds a block, and they cover [0, total_blocks)), since they then
-   travel as 12-byte records whose lengths follow from the next `first`.
-   ECAP otherwise (use flowkv_transfer_ex with a device plan); other
-   arguments and errors as for flowkv_transfer_ex. */
+   plan in device memory.  Up to FLOWKV_INLINE_RUNS records fit.  A plan in
+   the planner's form (record i starts where record i - 1 ends, every record
+   holds a block, and they cover [0, total_blocks)) travels as 12-byte
+   records whose lengths follow from the next `first`, so more fit: up to
+   FLOWKV_INLINE_RUNS_BLOCK_MAJOR between two block-major pools (one base
+   pointer per side), and up to FLOWKV_INLINE_RUNS_LAYER_MAJOR when either
+   pool is layer-major and the pools have at most FLOWKV_INLINE_LAYERS
+   layers (one base pointer per layer and side); flowkv_inline_capacity
+   gives the figure for two pools.  ECAP otherwise (use flowkv_transfer_ex
+   with a device plan); other arguments and errors as for
+   flowkv_transfer_ex. */
 int flowkv_transfer_inline(const flowkv_pool* src, const flowkv_pool* dst,
                            const flowkv_segment* segs_host, int64_t n_segs,
                            int64_t total_blocks, const flowkv_launch_config* cfg,
                            void* hip_stream);
+
+/* The most records of a planner-form plan (as flowkv_plan writes them) that
+   flowkv_transfer_inline carries between pools src and dst:
+   FLOWKV_INLINE_RUNS_BLOCK_MAJOR between two block-major pools, else
+   FLOWKV_INLINE_RUNS_LAYER_MAJOR when neither pool has more than
+   FLOWKV_INLINE_LAYERS layers, else FLOWKV_INLINE_RUNS.  Host only, no GPU
+   call.  EINVAL for NULL arguments, an unknown layout or num_layers outside
+   1..FLOWKV_MAX_LAYERS (*runs untouched). */
+int flowkv_inline_capacity(const flowkv_pool* src, const flowkv_pool* dst, int64_t* runs);
 
 /* Move one request (section 3.1's problem statement: K and V of request R
    from the sender's pool to the receiver's) in one call: flowkv_plan of src_ids
@@ -272,8 +288,8 @@ int flowkv_transfer_inline(const flowkv_pool* src, const flowkv_pool* dst,
    descriptors), then flowkv_transfer_inline with that plan.  *n_runs
    receives the plan's run count.  ECAP, with *n_runs set and nothing
    launched, when the plan has more runs than flowkv_transfer_inline carries
-   between these pools (then plan with flowkv_plan and launch with a device
-   plan).  Errors of the planner (ERANGE, EDUP) come before any launch; the
+   between these pools (flowkv_inline_capacity; then plan with flowkv_plan
+   and launch with a device plan).  Errors of the planner (ERANGE, EDUP) come before any launch; the
    others are flowkv_transfer_inline's.  n_blocks == 0 is a no-op. */
 int flowkv_transfer_request(const flowkv_pool* src, const flowkv_pool* dst,
                             const int32_t* src_ids, const int32_t* dst_ids, int32_t n_blocks,

@@ -18,9 +18,12 @@ extern "C" int flowkv_transfer_request(const flowkv_pool* src, const flowkv_pool
                                        int64_t* n_runs, void* hip_stream) {
   if (!src || !dst || !n_runs) return fail(FLOWKV_EINVAL, "NULL pool or n_runs");
   if (n_blocks < 0) return fail(FLOWKV_EINVAL, "negative block count %d", n_blocks);
-  const bool both_bm = src->layout == FLOWKV_LAYOUT_BLOCK_MAJOR &&
-                       dst->layout == FLOWKV_LAYOUT_BLOCK_MAJOR;
-  const int64_t cap = both_bm ? FLOWKV_INLINE_RUNS_BLOCK_MAJOR : FLOWKV_INLINE_RUNS;
+  int64_t cap = 0;
+  const int rcap = flowkv_inline_capacity(src, dst, &cap);
+  if (rcap) return rcap;
+  static_assert(FLOWKV_INLINE_RUNS_BLOCK_MAJOR >= FLOWKV_INLINE_RUNS_LAYER_MAJOR &&
+                    FLOWKV_INLINE_RUNS_BLOCK_MAJOR >= FLOWKV_INLINE_RUNS,
+                "the stack buffer holds the largest inline plan");
   flowkv_segment runs[FLOWKV_INLINE_RUNS_BLOCK_MAJOR];
   int64_t k = 0;
   const int rc = flowkv_plan(src_ids, dst_ids, n_blocks, src->num_blocks, dst->num_blocks, runs,

@@ -87,26 +87,35 @@ constexpr size_t kImplicitArgBytes = 256;
 static_assert(sizeof(XferArgs) + kImplicitArgBytes <= 4096,
               "kernel arguments must stay within 4 KiB");
 
-// Block-major pools on both sides need one base pointer each, which leaves
-// the kernel arguments room for longer plans in the planner's contiguous
-// form: 12-byte records, a run's length being the next record's `first`
-// minus its own (total_blocks for the last).
+// A plan in the planner's form (each run starting where the previous one
+// ends) travels as 12-byte records, a run's length being the next record's
+// `first` minus its own (total_blocks for the last).  With fewer base
+// pointers than FLOWKV_MAX_LAYERS per side the kernel arguments hold longer
+// plans: one pointer per side between block-major pools, one per layer (at
+// most FLOWKV_INLINE_LAYERS) when a pool is layer-major.
 struct CompactRun {
   int32_t src_block, dst_block, first;
 };
-constexpr int kInlineRunsBM = FLOWKV_INLINE_RUNS_BLOCK_MAJOR;
 
-struct PoolArgBM {
-  char* base[1];
+template <int kBases>
+struct PoolArgN {
+  char* base[kBases];
   int64_t num_blocks;
 };
 
-struct XferArgsBM : XferShape {
-  PoolArgBM src;
-  PoolArgBM dst;
-  CompactRun inline_runs[kInlineRunsBM];
+template <int kBases, int kRuns>
+struct XferArgsCompact : XferShape {
+  static constexpr int kMaxBases = kBases;
+  static constexpr int kMaxRuns = kRuns;
+  PoolArgN<kBases> src;
+  PoolArgN<kBases> dst;
+  CompactRun inline_runs[kRuns];
 };
+using XferArgsBM = XferArgsCompact<1, FLOWKV_INLINE_RUNS_BLOCK_MAJOR>;
+using XferArgsLM = XferArgsCompact<FLOWKV_INLINE_LAYERS, FLOWKV_INLINE_RUNS_LAYER_MAJOR>;
 static_assert(sizeof(XferArgsBM) + kImplicitArgBytes <= 4096,
+              "kernel arguments must stay within 4 KiB");
+static_assert(sizeof(XferArgsLM) + kImplicitArgBytes <= 4096,
               "kernel arguments must stay within 4 KiB");
 
 // Pool memory is global memory; naming the address space lets the compiler
@@ -269,15 +278,17 @@ __device__ __forceinline__ flowkv_segment run_at(const XferArgs& a, const cseg* 
   else return load_seg(segs + i);
 }
 
-// The compact inline form: the same records, each run ending where the next
-// one starts.
-template <bool kInline>
-__device__ __forceinline__ int32_t run_first(const XferArgsBM& a, const cseg*, int32_t i) {
+// The compact inline forms: the same records, each run ending where the
+// next one starts.
+template <bool kInline, int B, int R>
+__device__ __forceinline__ int32_t run_first(const XferArgsCompact<B, R>& a, const cseg*,
+                                             int32_t i) {
   return a.inline_runs[i].first;
 }
 
-template <bool kInline>
-__device__ __forceinline__ flowkv_segment run_at(const XferArgsBM& a, const cseg*, int32_t i) {
+template <bool kInline, int B, int R>
+__device__ __forceinline__ flowkv_segment run_at(const XferArgsCompact<B, R>& a, const cseg*,
+                                                 int32_t i) {
   const CompactRun r = a.inline_runs[i];
   const int32_t end = i + 1 < a.n_segs ? a.inline_runs[i + 1].first : int32_t(a.total_blocks);
   return flowkv_segment{r.src_block, r.dst_block, end - r.first, r.first};
@@ -397,39 +408,42 @@ __global__ __launch_bounds__(1024) void kv_segment_copy(const A a) {
   }
 }
 
-using KernelFn = void (*)(XferArgs);
+template <class A>
+using KernelOf = void (*)(A);
+using KernelFn = KernelOf<XferArgs>;
 
-template <bool S, bool D, int U, int C, bool I>
-KernelFn pick_path(bool uniform) {
-  return uniform ? kv_segment_copy<S, D, U, C, true, I> : kv_segment_copy<S, D, U, C, false, I>;
+template <class A, bool S, bool D, int U, int C, bool I>
+KernelOf<A> pick_path(bool uniform) {
+  return uniform ? kv_segment_copy<S, D, U, C, true, I, A>
+                 : kv_segment_copy<S, D, U, C, false, I, A>;
 }
 
-template <bool S, bool D, int U, bool I>
-KernelFn pick_cache(int cache, bool uniform) {
+template <class A, bool S, bool D, int U, bool I>
+KernelOf<A> pick_cache(int cache, bool uniform) {
   switch (cache) {
-    case 0: return pick_path<S, D, U, 0, I>(uniform);
-    case 1: return pick_path<S, D, U, 1, I>(uniform);
-    case 2: return pick_path<S, D, U, 2, I>(uniform);
-    default: return pick_path<S, D, U, 3, I>(uniform);
+    case 0: return pick_path<A, S, D, U, 0, I>(uniform);
+    case 1: return pick_path<A, S, D, U, 1, I>(uniform);
+    case 2: return pick_path<A, S, D, U, 2, I>(uniform);
+    default: return pick_path<A, S, D, U, 3, I>(uniform);
   }
 }
 
-template <bool S, bool D, bool I>
-KernelFn pick_unroll(int unroll, int cache, bool uniform) {
+template <class A, bool S, bool D, bool I>
+KernelOf<A> pick_unroll(int unroll, int cache, bool uniform) {
   switch (unroll) {
-    case 2: return pick_cache<S, D, 2, I>(cache, uniform);
-    case 4: return pick_cache<S, D, 4, I>(cache, uniform);
-    case 8: return pick_cache<S, D, 8, I>(cache, uniform);
-    default: return pick_cache<S, D, 16, I>(cache, uniform);
+    case 2: return pick_cache<A, S, D, 2, I>(cache, uniform);
+    case 4: return pick_cache<A, S, D, 4, I>(cache, uniform);
+    case 8: return pick_cache<A, S, D, 8, I>(cache, uniform);
+    default: return pick_cache<A, S, D, 16, I>(cache, uniform);
   }
 }
 
 template <bool I>
 KernelFn pick_layouts(bool src_lm, bool dst_lm, int unroll, int cache, bool uniform) {
-  if (src_lm && dst_lm) return pick_unroll<true, true, I>(unroll, cache, uniform);
-  if (src_lm) return pick_unroll<true, false, I>(unroll, cache, uniform);
-  if (dst_lm) return pick_unroll<false, true, I>(unroll, cache, uniform);
-  return pick_unroll<false, false, I>(unroll, cache, uniform);
+  if (src_lm && dst_lm) return pick_unroll<XferArgs, true, true, I>(unroll, cache, uniform);
+  if (src_lm) return pick_unroll<XferArgs, true, false, I>(unroll, cache, uniform);
+  if (dst_lm) return pick_unroll<XferArgs, false, true, I>(unroll, cache, uniform);
+  return pick_unroll<XferArgs, false, false, I>(unroll, cache, uniform);
 }
 
 KernelFn pick_kernel(bool src_lm, bool dst_lm, int unroll, int cache, bool uniform, bool inl) {
@@ -437,32 +451,51 @@ KernelFn pick_kernel(bool src_lm, bool dst_lm, int unroll, int cache, bool unifo
              : pick_layouts<false>(src_lm, dst_lm, unroll, cache, uniform);
 }
 
-// The compact inline form (block-major pools on both sides).
-using KernelFnBM = void (*)(XferArgsBM);
-
-template <int U, int C>
-KernelFnBM pick_bm_path(bool uniform) {
-  return uniform ? kv_segment_copy<false, false, U, C, true, true, XferArgsBM>
-                 : kv_segment_copy<false, false, U, C, false, true, XferArgsBM>;
+// The compact inline forms: block-major pools on both sides, or a
+// layer-major pool on at least one side.
+KernelOf<XferArgsBM> pick_kernel_bm(int unroll, int cache, bool uniform) {
+  return pick_unroll<XferArgsBM, false, false, true>(unroll, cache, uniform);
 }
 
-template <int U>
-KernelFnBM pick_bm_cache(int cache, bool uniform) {
-  switch (cache) {
-    case 0: return pick_bm_path<U, 0>(uniform);
-    case 1: return pick_bm_path<U, 1>(uniform);
-    case 2: return pick_bm_path<U, 2>(uniform);
-    default: return pick_bm_path<U, 3>(uniform);
-  }
+KernelOf<XferArgsLM> pick_kernel_lm(bool src_lm, bool dst_lm, int unroll, int cache,
+                                    bool uniform) {
+  if (src_lm && dst_lm) return pick_unroll<XferArgsLM, true, true, true>(unroll, cache, uniform);
+  if (src_lm) return pick_unroll<XferArgsLM, true, false, true>(unroll, cache, uniform);
+  return pick_unroll<XferArgsLM, false, true, true>(unroll, cache, uniform);
 }
 
-KernelFnBM pick_kernel_bm(int unroll, int cache, bool uniform) {
-  switch (unroll) {
-    case 2: return pick_bm_cache<2>(cache, uniform);
-    case 4: return pick_bm_cache<4>(cache, uniform);
-    case 8: return pick_bm_cache<8>(cache, uniform);
-    default: return pick_bm_cache<16>(cache, uniform);
+// Planner-form records the kernel arguments carry between two pools whose
+// descriptors have been checked (0: only the general form).
+int64_t compact_capacity(const flowkv_pool* src, const flowkv_pool* dst) {
+  if (src->layout == FLOWKV_LAYOUT_BLOCK_MAJOR && dst->layout == FLOWKV_LAYOUT_BLOCK_MAJOR)
+    return XferArgsBM::kMaxRuns;
+  if (src->num_layers <= XferArgsLM::kMaxBases && dst->num_layers <= XferArgsLM::kMaxBases)
+    return XferArgsLM::kMaxRuns;
+  return 0;
+}
+
+// The compact arguments from the general ones and the planner's records.
+template <class C>
+C compact_args(const XferArgs& a, const flowkv_segment* runs, int64_t n) {
+  C c{};
+  static_cast<XferShape&>(c) = static_cast<const XferShape&>(a);
+  const int nb = a.num_layers < C::kMaxBases ? a.num_layers : C::kMaxBases;
+  for (int i = 0; i < nb; ++i) {
+    c.src.base[i] = a.src.base[i];
+    c.dst.base[i] = a.dst.base[i];
   }
+  c.src.num_blocks = a.src.num_blocks;
+  c.dst.num_blocks = a.dst.num_blocks;
+  for (int64_t i = 0; i < n; ++i)
+    c.inline_runs[i] = CompactRun{runs[i].src_block, runs[i].dst_block, runs[i].first};
+  return c;
+}
+
+template <class A>
+hipError_t launch_kernel(KernelOf<A> fn, A& args, int64_t grid, int threads, void* stream) {
+  void* p[] = {&args};
+  return hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(grid)),
+                         dim3(unsigned(threads)), p, 0, static_cast<hipStream_t>(stream));
 }
 
 // True when the records are the planner's form: run i starts where run i-1
@@ -611,15 +644,20 @@ int launch_transfer(const flowkv_pool* src, const flowkv_pool* dst,
   if (cache < 1 || cache > 4) return fail(FLOWKV_EINVAL, "cache %d: need 1..4", cache);
   if (grid < 0) return fail(FLOWKV_EINVAL, "negative grid %d", grid);
   const bool inl = segs_host != nullptr;
-  // more than kInlineRuns records ride in the kernel arguments only in the
-  // compact form: block-major pools on both sides, the planner's records
+  // more than kInlineRuns records ride in the kernel arguments only in a
+  // compact form: the planner's records, between pools that need few base
+  // pointers
   bool compact = false;
   if (inl && n_segs > kInlineRuns) {
-    if (!both_bm || n_segs > kInlineRunsBM)
+    const int64_t cap = compact_capacity(src, dst);
+    if (n_segs > cap)
       return fail(FLOWKV_ECAP,
-                  "%lld runs: at most %d travel in the kernel arguments (%d between "
-                  "block-major pools)",
-                  (long long)n_segs, kInlineRuns, kInlineRunsBM);
+                  "%lld runs: at most %lld travel in the kernel arguments between these pools "
+                  "(%d for any plan; as the planner writes them, %d between block-major pools, "
+                  "%d between pools of at most %d layers)",
+                  (long long)n_segs, (long long)(cap > kInlineRuns ? cap : kInlineRuns),
+                  kInlineRuns, XferArgsBM::kMaxRuns, XferArgsLM::kMaxRuns,
+                  XferArgsLM::kMaxBases);
     if (!contiguous_plan(segs_host, n_segs, total_blocks))
       return fail(FLOWKV_ECAP,
                   "%lld runs: beyond %d, a plan travels in the kernel arguments only as the "
@@ -686,28 +724,19 @@ int launch_transfer(const flowkv_pool* src, const flowkv_pool* dst,
   }
   launch = std::min<int64_t>(launch, INT32_MAX);
 
+  const bool src_lm = src->layout == FLOWKV_LAYOUT_LAYER_MAJOR;
+  const bool dst_lm = dst->layout == FLOWKV_LAYOUT_LAYER_MAJOR;
   hipError_t e;
-  if (compact) {
-    XferArgsBM b{};
-    static_cast<XferShape&>(b) = static_cast<const XferShape&>(a);
-    b.src.base[0] = a.src.base[0];
-    b.src.num_blocks = a.src.num_blocks;
-    b.dst.base[0] = a.dst.base[0];
-    b.dst.num_blocks = a.dst.num_blocks;
-    for (int64_t i = 0; i < n_segs; ++i)
-      b.inline_runs[i] = CompactRun{segs_host[i].src_block, segs_host[i].dst_block,
-                                    segs_host[i].first};
-    KernelFnBM fn = pick_kernel_bm(unroll, cache - 1, uniform);
-    void* args[] = {&b};
-    e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(launch)),
-                        dim3(unsigned(threads)), args, 0, static_cast<hipStream_t>(hip_stream));
+  if (compact && both_bm) {
+    XferArgsBM c = compact_args<XferArgsBM>(a, segs_host, n_segs);
+    e = launch_kernel(pick_kernel_bm(unroll, cache - 1, uniform), c, launch, threads, hip_stream);
+  } else if (compact) {
+    XferArgsLM c = compact_args<XferArgsLM>(a, segs_host, n_segs);
+    e = launch_kernel(pick_kernel_lm(src_lm, dst_lm, unroll, cache - 1, uniform), c, launch,
+                      threads, hip_stream);
   } else {
-    KernelFn fn = pick_kernel(src->layout == FLOWKV_LAYOUT_LAYER_MAJOR,
-                              dst->layout == FLOWKV_LAYOUT_LAYER_MAJOR, unroll, cache - 1,
-                              uniform, inl);
-    void* args[] = {&a};
-    e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(launch)),
-                        dim3(unsigned(threads)), args, 0, static_cast<hipStream_t>(hip_stream));
+    e = launch_kernel(pick_kernel(src_lm, dst_lm, unroll, cache - 1, uniform, inl), a, launch,
+                      threads, hip_stream);
   }
   if (e == hipSuccess) e = hipGetLastError();
   if (e != hipSuccess) return fail(FLOWKV_EHIP, "kernel launch: %s", hipGetErrorString(e));
@@ -732,6 +761,22 @@ extern "C" int flowkv_transfer_inline(const flowkv_pool* src, const flowkv_pool*
   static const flowkv_segment none{};
   return launch_transfer(src, dst, nullptr, segs_host ? segs_host : &none, n_segs, total_blocks,
                          0, 0, true, cfg, hip_stream);
+}
+
+extern "C" int flowkv_inline_capacity(const flowkv_pool* src, const flowkv_pool* dst,
+                                      int64_t* runs) {
+  if (!src || !dst || !runs) return fail(FLOWKV_EINVAL, "NULL pool or output");
+  const flowkv_pool* p[2] = {src, dst};
+  for (const flowkv_pool* q : p) {
+    if (q->layout != FLOWKV_LAYOUT_LAYER_MAJOR && q->layout != FLOWKV_LAYOUT_BLOCK_MAJOR)
+      return fail(FLOWKV_EINVAL, "unknown layout %d", q->layout);
+    if (q->num_layers < 1 || q->num_layers > FLOWKV_MAX_LAYERS)
+      return fail(FLOWKV_EINVAL, "num_layers %d outside 1..%d", q->num_layers,
+                  FLOWKV_MAX_LAYERS);
+  }
+  const int64_t cap = compact_capacity(src, dst);
+  *runs = cap > kInlineRuns ? cap : kInlineRuns;
+  return ok();
 }
 
 extern "C" int flowkv_transfer_layers(const flowkv_pool* src, const flowkv_pool* dst,

@@ -26,6 +26,8 @@ LAYOUT_LAYER_MAJOR, LAYOUT_BLOCK_MAJOR = 0, 1
 MAX_LAYERS = 128
 INLINE_RUNS = 64  # plan records flowkv_transfer_inline carries in the kernel arguments
 INLINE_RUNS_BLOCK_MAJOR = 300  # ... between two block-major pools, in the planner's form
+INLINE_LAYERS = 32  # pools of at most this many layers ...
+INLINE_RUNS_LAYER_MAJOR = 264  # ... carry this many planner-form records when one is layer-major
 
 SEGMENT_DTYPE = np.dtype([("src_block", "<i4"), ("dst_block", "<i4"),
                           ("n_blocks", "<i4"), ("first", "<i4")])
@@ -103,6 +105,7 @@ SIGNATURES = {
     "flowkv_transfer_inline": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_int64,
                                               ctypes.c_int64, ctypes.POINTER(flowkv_launch_config),
                                               ctypes.c_void_p]),
+    "flowkv_inline_capacity": (ctypes.c_int, [_POOLP, _POOLP, _I64P]),
     "flowkv_transfer_request": (ctypes.c_int, [_POOLP, _POOLP, ctypes.c_void_p, ctypes.c_void_p,
                                                ctypes.c_int32,
                                                ctypes.POINTER(flowkv_launch_config), _I64P,
@@ -485,8 +488,10 @@ def flowkv_transfer_ex(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_bl
 def inline_capacity(src: KVPool, dst: KVPool) -> int:
     """Most plan records (as flowkv_plan writes them) that flowkv_transfer_inline
     carries in the kernel arguments between these two pools."""
-    both_bm = src.layout == LAYOUT_BLOCK_MAJOR and dst.layout == LAYOUT_BLOCK_MAJOR
-    return INLINE_RUNS_BLOCK_MAJOR if both_bm else INLINE_RUNS
+    n = ctypes.c_int64()
+    _check(_lib.flowkv_inline_capacity(ctypes.byref(src.desc), ctypes.byref(dst.desc),
+                                       ctypes.byref(n)), "flowkv_inline_capacity")
+    return n.value
 
 
 def flowkv_transfer_inline(src: KVPool, dst: KVPool, segs: np.ndarray, total_blocks: int,
@@ -494,8 +499,9 @@ def flowkv_transfer_inline(src: KVPool, dst: KVPool, segs: np.ndarray, total_blo
                            order: int = 0, stream=None) -> None:
     """Enqueue the one-launch copy with a host plan (SEGMENT_DTYPE array, or
     int (k, 4) rows) carried in the kernel arguments: at most INLINE_RUNS
-    records, or INLINE_RUNS_BLOCK_MAJOR in the planner's form between
-    block-major pools (``inline_capacity``)."""
+    records; in the planner's form, INLINE_RUNS_BLOCK_MAJOR between
+    block-major pools, or INLINE_RUNS_LAYER_MAJOR when a pool is layer-major
+    and neither has more than INLINE_LAYERS layers (``inline_capacity``)."""
     segs = _host_segments(segs)
     cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
     _check(_lib.flowkv_transfer_inline(ctypes.byref(src.desc), ctypes.byref(dst.desc),

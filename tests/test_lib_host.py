@@ -27,6 +27,35 @@ def declared_functions():
     return sorted(set(re.findall(r"\b(flowkv_\w+)\s*\(", text)))
 
 
+def test_inline_capacity_by_layouts_and_depth():
+    """flowkv_inline_capacity: the compact forms' limits, host only."""
+    def cap(s, d):
+        n = ctypes.c_int64(-9)
+        rc = fk.lib().flowkv_inline_capacity(ctypes.byref(s), ctypes.byref(d), ctypes.byref(n))
+        return rc, n.value
+
+    for L in (1, 2, fk.INLINE_LAYERS, fk.INLINE_LAYERS + 1, fk.MAX_LAYERS):
+        lm = pool(layout=0, L=L, bases=tuple(range(1 << 20, (1 << 20) + L)))
+        bm = pool(layout=1, L=L)
+        few = L <= fk.INLINE_LAYERS
+        want_lm = fk.INLINE_RUNS_LAYER_MAJOR if few else fk.INLINE_RUNS
+        assert cap(bm, bm) == (fk.OK, fk.INLINE_RUNS_BLOCK_MAJOR), L
+        assert cap(lm, bm) == (fk.OK, want_lm), L
+        assert cap(bm, lm) == (fk.OK, want_lm), L
+        assert cap(lm, lm) == (fk.OK, want_lm), L
+    # the deeper pool decides
+    assert cap(pool(layout=0, L=2, bases=(1, 2)), pool(layout=1, L=fk.INLINE_LAYERS + 1)) == \
+        (fk.OK, fk.INLINE_RUNS)
+    # errors leave the output alone
+    for s in (pool(layout=7), pool(L=0), pool(L=fk.MAX_LAYERS + 1)):
+        assert cap(s, pool()) == (fk.EINVAL, -9)
+        assert cap(pool(), s) == (fk.EINVAL, -9)
+    n = ctypes.c_int64()
+    assert fk.lib().flowkv_inline_capacity(None, ctypes.byref(pool()), ctypes.byref(n)) == fk.EINVAL
+    assert fk.lib().flowkv_inline_capacity(ctypes.byref(pool()), ctypes.byref(pool()), None) == \
+        fk.EINVAL
+
+
 def test_library_exports_every_declared_function():
     names = declared_functions()
     assert len(names) >= 12
@@ -41,6 +70,8 @@ def test_binding_constants_match_the_header():
     defines = dict(re.findall(r"#define\s+(FLOWKV_\w+)\s+(-?\d+)", text))
     assert int(defines["FLOWKV_INLINE_RUNS"]) == fk.INLINE_RUNS
     assert int(defines["FLOWKV_INLINE_RUNS_BLOCK_MAJOR"]) == fk.INLINE_RUNS_BLOCK_MAJOR
+    assert int(defines["FLOWKV_INLINE_LAYERS"]) == fk.INLINE_LAYERS
+    assert int(defines["FLOWKV_INLINE_RUNS_LAYER_MAJOR"]) == fk.INLINE_RUNS_LAYER_MAJOR
     assert int(defines["FLOWKV_ATTN_SCRATCH_BYTES"]) == fk.ATTN_SCRATCH_BYTES
     enums = dict(re.findall(r"\b(FLOWKV_E?\w+)\s*=\s*(-?\d+)", text))
     for name in ("OK", "EINVAL", "ENOSPC", "ERANGE", "EDUP", "ECAP", "EHIP", "ENOMEM"):
@@ -588,8 +619,18 @@ def test_transfer_rejects_bad_pools_without_touching_the_device():
     assert inline(good_src, good_dst, planner_form(fk.INLINE_RUNS_BLOCK_MAJOR + 1),
                   fk.INLINE_RUNS_BLOCK_MAJOR + 1) == fk.ECAP
     runs = planner_form(100)
+    # a layer-major pool: the compact form up to INLINE_RUNS_LAYER_MAJOR
+    # records while neither pool has more than INLINE_LAYERS layers
     lm_src = pool(layout=0, L=2, bases=(1 << 34, (1 << 34) + (1 << 24)))
-    assert inline(lm_src, good_dst, runs, 100) == fk.ECAP        # layer-major sender
+    k = fk.INLINE_RUNS_LAYER_MAJOR + 1
+    assert inline(lm_src, good_dst, planner_form(k), k) == fk.ECAP
+    L = fk.INLINE_LAYERS + 1
+    deep = [pool(layout=lay, L=L, bases=tuple((1 << 36) * (j + 1) + (i << 24) for i in
+                                              range(L if lay == 0 else 1)))
+            for j, lay in enumerate((0, 1, 0))]
+    k = fk.INLINE_RUNS + 1
+    assert inline(deep[0], deep[1], planner_form(k), k) == fk.ECAP
+    assert inline(deep[1], deep[2], planner_form(k), k) == fk.ECAP
     gap = runs.copy()
     gap["first"][50] += 1
     assert inline(good_src, good_dst, gap, 100) == fk.ECAP       # runs do not abut
@@ -635,7 +676,14 @@ def test_transfer_request_rejects_before_any_device_call():
     assert req(bm, bm, [0, 1], [5, 6]) == (fk.EINVAL, -1)           # n_runs left untouched
     stride2 = 2 * np.arange(301)
     assert req(bm, bm2, stride2, stride2 + 1) == (fk.ECAP, 301)      # block-major: 300 fit
-    assert req(bm, lm, np.arange(65) * 2, np.arange(65) * 2) == (fk.ECAP, 65)   # else 64
+    k = fk.INLINE_RUNS_LAYER_MAJOR + 1                                # a layer-major pool
+    assert req(bm, lm, np.arange(k) * 2, np.arange(k) * 2) == (fk.ECAP, k)
+    L = fk.INLINE_LAYERS + 1                                         # ... of many layers
+    bm_deep = pool(layout=1, L=L, B=1000, bases=(1 << 31,))
+    lm_deep = pool(layout=0, L=L, B=1000, bases=tuple((1 << 32) + (i << 24) for i in range(L)))
+    k = fk.INLINE_RUNS + 1
+    assert req(bm_deep, lm_deep, np.arange(k) * 2, np.arange(k) * 2) == (fk.ECAP, k)
+    assert req(lm, pool(layout=7), [0], [0]) == (fk.EINVAL, -1)      # bad pool: no planning
 
 
 def test_abi_check_program_is_built_and_runs_without_python():

@@ -397,18 +397,22 @@ def test_inline_plans_against_oracle(seed):
     assert host_equal(download_all(dst), h_dst)
 
 
-@pytest.mark.parametrize("seed", range(10))
+@pytest.mark.parametrize("seed", range(16))
 def test_compact_inline_plans_against_oracle(seed):
-    """Plans of 65 to 300 runs between block-major pools, carried in the
-    kernel arguments as 12-byte records: random geometries (both the uniform
-    and the per-lane path), runs of 1 to 3 blocks, random launch shapes."""
+    """Plans of 65 runs up to the compact capacity, carried in the kernel
+    arguments as 12-byte records: 300 between block-major pools, 264 when a
+    pool is layer-major (at most 32 layers); every layout pair, random
+    geometries (the uniform and the per-lane path, 1 to 32 layers), runs of
+    1 to 3 blocks, random launch shapes."""
     g = np.random.default_rng(5000 + seed)
     geoms = [Geometry("c1", 2, 2, 64, 16, "float16"), Geometry("c2", 3, 3, 40, 16, "bfloat16"),
-             Geometry("c3", 1, 1, 128, 5, "float16")]
+             Geometry("c3", 1, 1, 128, 5, "float16"), Geometry("c4", 32, 1, 32, 2, "bfloat16")]
     geom = geoms[seed % len(geoms)]
-    k = int(g.integers(fk.INLINE_RUNS + 1, fk.INLINE_RUNS_BLOCK_MAJOR + 1))
-    if seed == 0:
-        k = fk.INLINE_RUNS_BLOCK_MAJOR
+    sl, dl = LAYOUT_PAIRS[(seed // len(geoms)) % 4]
+    cap = fk.INLINE_RUNS_BLOCK_MAJOR if (sl, dl) == (BM, BM) else fk.INLINE_RUNS_LAYER_MAJOR
+    k = int(g.integers(fk.INLINE_RUNS + 1, cap + 1))
+    if seed < 4:
+        k = cap
     lens = g.integers(1, 4, size=k)
     n = int(lens.sum())
     B = 2 * n + 8
@@ -424,9 +428,11 @@ def test_compact_inline_plans_against_oracle(seed):
     segs = fk.flowkv_plan(S, D, B, B)
     assert len(segs) == k
     cfg = CONFIGS[seed % len(CONFIGS)]
-    say(f"compact inline seed={seed} runs={k} blocks={n} geom={geom.name} cfg={cfg}")
-    src = device_pool(geom, BM, B, seed)
-    dst = device_pool(geom, BM, B, seed + 1)
+    say(f"compact inline seed={seed} {NAMES[sl]}->{NAMES[dl]} runs={k} blocks={n} "
+        f"geom={geom.name} cfg={cfg}")
+    src = device_pool(geom, sl, B, seed)
+    dst = device_pool(geom, dl, B, seed + 1)
+    assert fk.inline_capacity(src, dst) == cap
     h_src, h_dst = download_all(src), download_all(dst)
     fk.flowkv_transfer_inline(src, dst, segs, n, **cfg)
     torch.cuda.synchronize()
@@ -498,21 +504,27 @@ def test_inline_plan_at_the_limit_equals_device_plan():
     assert host_equal(got, download_all(d2))
 
 
-def test_compact_inline_plan_at_the_limit_equals_device_plan():
-    """300 one-block runs (the block-major inline limit) at the 8B geometry:
-    the compact inline plan and the device-memory plan give the same receiver
-    pool, and match the oracle."""
+@pytest.mark.parametrize("sl,dl", [(BM, BM), (LM, LM), (BM, LM)], ids=lambda x: NAMES[x])
+def test_compact_inline_plan_at_the_limit_equals_device_plan(sl, dl):
+    """One-block runs up to the compact limit (300 between block-major
+    pools, 264 with a layer-major pool) at the 8B geometry, whose 32 layers
+    fill the layer-major form's base pointers: the compact inline plan and
+    the device-memory plan give the same receiver pool, and match the
+    oracle."""
     geom = LLAMA3_8B
-    k = fk.INLINE_RUNS_BLOCK_MAJOR
+    assert geom.num_layers == fk.INLINE_LAYERS
+    k = fk.INLINE_RUNS_BLOCK_MAJOR if (sl, dl) == (BM, BM) else fk.INLINE_RUNS_LAYER_MAJOR
     B = 2 * k + 2
-    src = device_pool(geom, BM, B, 0)
-    d1 = device_pool(geom, BM, B, 1)
-    d2 = device_pool(geom, BM, B, 1)
+    src = device_pool(geom, sl, B, 0)
+    d1 = device_pool(geom, dl, B, 1)
+    d2 = device_pool(geom, dl, B, 1)
+    assert fk.inline_capacity(src, d1) == k
     h_src, h_dst = download_all(src), download_all(d1)
     S = 2 * np.arange(k, dtype=np.int32)
     D = 2 * np.arange(k, dtype=np.int32) + 1
     segs = fk.flowkv_plan(S, D, B, B)
     assert len(segs) == k
+    say(f"compact inline at the limit {NAMES[sl]}->{NAMES[dl]}: {k} runs")
     fk.flowkv_transfer_inline(src, d1, segs, k)
     fk.flowkv_transfer(src, d2, fk.segments_to_device(segs, src.device), len(segs), k)
     torch.cuda.synchronize()
