@@ -453,9 +453,10 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
 //   - the next tile's K and V loads are issued right after this tile's q.k,
 //     into the wave's other V buffer, so they are in flight during this
 //     tile's softmax and P.V (4% faster on a 70B share, measured).  With
-//     the second buffer (78.6 KB of LDS in all) and 174 registers per lane,
-//     two workgroups fit on a CU, not three; none of the measured workloads
-//     ran slower for it.
+//     the second buffer (78.6 KB of LDS in all), two workgroups fit on a
+//     CU, not three: LDS, not the 168 registers per lane (136 vector, 32
+//     accumulation), sets that limit.  None of the measured workloads ran
+//     slower for it.
 // The waves' partial (max, sum, weighted V) merge through LDS at the end.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
