@@ -64,9 +64,12 @@ def first_mismatch(a: oracle.HostPool, b: oracle.HostPool):
     return None
 
 
-def run_transfer(src, dst, segs, stream=None, inline=False, **cfg):
-    """One launch of the plan: from device memory, or (inline) carried in
-    the kernel's arguments as bench.py sends plans of at most 64 runs."""
+def run_transfer(src, dst, segs, stream=None, inline=False, layerwise=False, **cfg):
+    """The plan moved as bench.py moves it: one launch with the plan in device
+    memory, or (inline) carried in the kernel's arguments, as bench.py sends
+    every plan that fits there (``fk.inline_capacity``); or (layerwise) one
+    launch per layer from device memory, as its Table 3 sweep times the
+    layer-wise form."""
     total = fk.plan_total_blocks(segs)
     if inline:
         fk.flowkv_transfer_inline(src, dst, segs, total, stream=stream, **cfg)
@@ -74,7 +77,11 @@ def run_transfer(src, dst, segs, stream=None, inline=False, **cfg):
         return None
     dev = fk.segments_to_device(segs, src.device) if len(segs) else torch.zeros(
         (0, 4), dtype=torch.int32, device=src.device)
-    if cfg:
+    if layerwise:
+        for layer in range(src.num_layers):
+            fk.flowkv_transfer_layers(src, dst, dev, len(segs), total, layer, 1, stream=stream,
+                                      **cfg)
+    elif cfg:
         fk.flowkv_transfer_ex(src, dst, dev, len(segs), total, stream=stream, **cfg)
     else:
         fk.flowkv_transfer(src, dst, dev, len(segs), total, stream=stream)
@@ -154,7 +161,7 @@ def block_checksums(pool: fk.KVPool, piece_bytes: int = 256 << 20) -> torch.Tens
 
 
 def check_sampled(wl, wl_ref, sl, dl, max_blocks=1536, untouched_frac=0.01, max_untouched=1024,
-                  seed_sample=7, inline=False, **cfg):
+                  seed_sample=7, inline=False, layerwise=False, **cfg):
     """Full-size comparison: a seeded sample of the moved blocks (all of them
     when there are at most max_blocks) against the oracle; every moved block
     against its sender block on the device (`moved_blocks_equal`); the guard
@@ -195,7 +202,7 @@ def check_sampled(wl, wl_ref, sl, dl, max_blocks=1536, untouched_frac=0.01, max_
     keep = np.unique(np.concatenate((guards[:max_untouched], rest))).astype(np.int64)
     before = download_blocks(dst, keep)
     sums_before = block_checksums(dst)
-    run_transfer(src, dst, segs, inline=inline, **cfg)
+    run_transfer(src, dst, segs, inline=inline, layerwise=layerwise, **cfg)
     untouched = torch.as_tensor(~touched, device=dst.device)
     sums_after = block_checksums(dst)
     changed = (sums_after != sums_before).any(1) & untouched

@@ -289,16 +289,35 @@ def test_llama8b_13k_full_size(policy, sl, dl):
 
 
 @pytest.mark.parametrize("policy,sl,dl", [("segment", BM, BM), ("segment", LM, BM),
-                                          ("fifo_sorted", BM, BM)])
+                                          ("fifo_sorted", BM, BM), ("fifo_sorted", LM, LM)])
 def test_llama8b_13k_full_size_plan_in_kernel_arguments(policy, sl, dl):
     """The 13k request in the launch bench.py times for it: the plan carried
     in the kernel's arguments -- 43 runs from the segment-allocator receiver,
-    255 (12-byte records, block-major pools) from the free-list receiver."""
+    255 from the free-list receiver (12-byte records beside one base pointer
+    per side between block-major pools, beside 32 per side between
+    layer-major ones)."""
     wl, ref = build(recipes.llama8b_13k, policy)
+    say(f"8b 13k inline {policy} {NAMES[sl]}->{NAMES[dl]}")
     segs, nb, nk = check_sampled(wl, ref, sl, dl, inline=True)
     assert nb == 813
-    assert len(segs) <= (fk.INLINE_RUNS_BLOCK_MAJOR if (sl, dl) == (BM, BM) else fk.INLINE_RUNS)
+    cap = (fk.INLINE_RUNS_BLOCK_MAJOR if (sl, dl) == (BM, BM) else fk.INLINE_RUNS_LAYER_MAJOR)
+    assert len(segs) <= cap
+    if policy == "fifo_sorted":
+        assert len(segs) > fk.INLINE_RUNS  # the compact form
     say(f"  inline: {len(segs)} runs, {nb} blocks checked, {nk} untouched checked")
+
+
+@pytest.mark.parametrize("tokens", [500, 4000, 12000])
+def test_table3_lengths_full_size_per_layer_launches(tokens):
+    """Table 3's FlowKV-Layerwise column as bench.py --op table3 times it:
+    the request at one of the table's input lengths, free-list receiver in
+    the 65,536-block pools, moved as 32 per-layer launches from a device
+    plan; sampled against the oracle like the other full-size cases."""
+    wl, ref = build(recipes.llama8b_13k, "fifo_sorted", 65_536, tokens)
+    say(f"table3 {tokens} tokens, per-layer launches: {wl.n_blocks} blocks")
+    segs, nb, nk = check_sampled(wl, ref, BM, BM, layerwise=True)
+    assert nb == wl.n_blocks
+    say(f"  {len(segs)} runs, {nb} blocks checked, {nk} untouched checked")
 
 
 @pytest.mark.parametrize("policy,sl,dl", [("segment", BM, BM), ("fifo_shuffled", BM, BM),
