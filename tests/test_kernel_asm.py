@@ -9,6 +9,9 @@ instructions per iteration -- the next tile's loads -- and nothing else that
 counts against the same counter (a register spill to scratch would).  The
 immediate comes from the constexpr counts that size the issue loop; this test
 checks the emitted code against it, for both layouts.
+
+The transfer kernels are checked the same way for what the library claims
+of them: every instantiation runs without scratch memory.
 """
 
 import os
@@ -80,3 +83,51 @@ def test_mfma_wait_matches_the_loads_the_loop_issues(asm, layout):
     meta = metadata(asm, name)
     assert re.search(r"\.private_segment_fixed_size:\s+0\b", meta)
     assert re.search(r"\.vgpr_spill_count:\s+0\b", meta)
+
+
+# ---- the transfer kernels: no scratch memory, no spills ------------------------
+
+XFER_SRC = os.path.join(ROOT, "paper_2504_03775_amd", "csrc", "flowkv_transfer.hip")
+
+
+@pytest.fixture(scope="module")
+def xfer_asm(tmp_path_factory):
+    cc = hipcc()
+    if cc is None:
+        pytest.skip("hipcc not found")
+    out = tmp_path_factory.mktemp("asm") / "xfer.s"
+    from paper_2504_03775_amd.build import HIP_FLAGS, INCLUDE, CSRC
+    flags = [f for f in HIP_FLAGS if f not in ("-fPIC", "-Wall")]
+    subprocess.run([cc, *flags, "--cuda-device-only", "-S", "-I", INCLUDE, "-I", CSRC, XFER_SRC,
+                    "-o", str(out)], check=True, capture_output=True, timeout=900)
+    return out.read_text()
+
+
+def test_transfer_kernels_use_no_scratch_and_spill_nothing(xfer_asm):
+    """Every instantiation of kv_segment_copy -- both layouts on each side,
+    every unroll and cache policy, both address paths, the device-plan form
+    and the three argument forms -- keeps its state in registers: no private
+    (scratch) segment and no vector registers spilled.  So the transfer needs
+    no device memory beyond the pools and the caller's plan, which is why it
+    has no variant that allocates nothing.  The default launch shape (unroll
+    4) spills no scalar registers either; some unroll-16 forms spill a few
+    into vector-register lanes, which costs no memory."""
+    names = re.findall(r"\.name:\s+(\S*kv_segment_copy\S*)", xfer_asm)
+    # 4 layout pairs x 4 unroll x 4 cache x 2 paths x (device plan, general
+    # inline form), 32 between block-major pools and 96 with a layer-major
+    # pool in the compact forms
+    assert len(names) == 4 * 4 * 4 * 2 * 2 + 32 + 96, len(names)
+    assert sum("XferArgsCompactILi1E" in n for n in names) == 32
+    assert sum("XferArgsCompactILi32E" in n for n in names) == 96
+    # the code object's kernel list, one YAML entry per kernel
+    entries = [e for e in re.split(r"\n  - ", xfer_asm) if "kv_segment_copy" in e
+               and re.search(r"\.name:\s+\S*kv_segment_copy", e)]
+    assert len(entries) == len(names)
+    for e in entries:
+        n = re.search(r"\.name:\s+(\S+)", e).group(1)
+        assert re.search(r"\.private_segment_fixed_size:\s+0\b", e), n
+        assert re.search(r"\.vgpr_spill_count:\s+0\b", e), n
+        if "ELi4ELi" in n:    # unroll 4, the default
+            assert re.search(r"\.sgpr_spill_count:\s+0\b", e), n
+        size = int(re.search(r"\.kernarg_segment_size:\s+(\d+)", e).group(1))
+        assert size <= 4096, (n, size)
