@@ -18,7 +18,7 @@
 // Work split (flash-decoding style):
 //   pass 1: one workgroup per (KV head, token split, request).  A token's
 //           head vector (Dh bf16) is read by one 16-lane DPP row, Dh/16
-//           values per lane; the workgroup's 16 rows take the split's tokens
+//           values per lane; the workgroup's 32 rows take the split's tokens
 //           round-robin, 4 tokens per row per step (with G = 8, two rows
 //           share each token, 4 query heads each).  The loads are
 //           branch-free, so their count per step is static.
@@ -63,9 +63,13 @@ typedef __attribute__((address_space(1))) u32x4 gvec4;
 typedef __attribute__((address_space(1))) u32x2 gvec2;
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kThreads = 256;              // pass-1 workgroup: 4 waves
+// Pass-1 workgroups: 8 waves on the vector units, 4 on the matrix cores.
+// (Eight waves per split, against four, took the 32-request batch from
+// 0.244 to 0.237 ms at its 1024-token splits, measured interleaved.)
+constexpr int kVecThreads = 512;
+constexpr int kMfmaThreads = 256;
 constexpr int kRowLanes = 16;              // lanes per token: one DPP row
-constexpr int kRows = kThreads / kRowLanes;
+constexpr int kRows = kVecThreads / kRowLanes;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLazy = 8.f;               // log2 of the largest unnormalised weight
 
@@ -158,7 +162,7 @@ template <> struct Words<2> {
 };
 
 template <int kDh, int kG, bool kLM>
-__global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) {
+__global__ __launch_bounds__(kVecThreads) void decode_attn_split(const AttnArgs a) {
   constexpr int kW = kDh / 32;                  // bf16 pairs per lane (4 or 2)
   constexpr int kV = 2 * kW;                    // K/V values per lane
   constexpr int kTok = 4;                       // tokens per row per step
@@ -195,7 +199,7 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
   {
     const int span = (t0 + a.split_tokens - 1) / bs - b0 + 1;
     const int nb = span < a.max_blocks - b0 ? span : a.max_blocks - b0;
-    for (int i = tid; i < nb; i += kThreads)
+    for (int i = tid; i < nb; i += kVecThreads)
       s_blk[i] = a.tables[int64_t(r) * a.max_blocks + b0 + i];
   }
   const int T = clamp_len(a, a.seq_lens[r]);
@@ -381,7 +385,7 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
   // each row's reference max m_row against the largest M; a row that saw no
   // token has m_row = -inf and weighs nothing
   __shared__ float s_m[kRows][kGl], s_l[kRows][kGl], s_w[kRows][kGl];
-  __shared__ __attribute__((aligned(16))) float s_acc[kThreads / 64][kG][kDh];
+  __shared__ __attribute__((aligned(16))) float s_acc[kVecThreads / 64][kG][kDh];
 #pragma unroll
   for (int j = 0; j < kR; ++j) {
     float l = lsum[j];
@@ -410,7 +414,7 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
   }
   __syncthreads();
   // weight each row's sums, add the rows of a wave that share heads (lane
-  // distance 16 x kHS), then the 4 waves
+  // distance 16 x kHS), then the waves
   const int wave = tid / 64, row_in_wave = row % 4;
 #pragma unroll
   for (int h = 0; h < kGl; ++h) {
@@ -424,11 +428,11 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split(const AttnArgs a) 
     }
   }
   __syncthreads();
-  for (int i = tid; i < kG * kDh; i += kThreads) {
+  for (int i = tid; i < kG * kDh; i += kVecThreads) {
     const int h = i / kDh, d = i % kDh;
     float A = 0.f;
 #pragma unroll
-    for (int x = 0; x < kThreads / 64; ++x) A += s_acc[x][h][d];
+    for (int x = 0; x < kVecThreads / 64; ++x) A += s_acc[x][h][d];
     dst0[h * head_stride + 2 + d] = A;
   }
 }
@@ -465,9 +469,9 @@ template <int kCtrl>
 __device__ __forceinline__ float dpp_max(float x) { return fmaxf(x, dpp<kCtrl>(x)); }
 
 template <int kG, bool kLM>
-__global__ __launch_bounds__(kThreads) void decode_attn_split_mfma(const AttnArgs a) {
+__global__ __launch_bounds__(kMfmaThreads) void decode_attn_split_mfma(const AttnArgs a) {
   constexpr int kDh = 128;
-  constexpr int kWaves = kThreads / 64;
+  constexpr int kWaves = kMfmaThreads / 64;
   constexpr int kTile = 32;                      // tokens per wave step
   constexpr int kVBytes = 8 * 1024;              // LDS bytes of a wave's V tile
   constexpr int kStep = kWaves * kTile;          // tokens per workgroup step
@@ -493,7 +497,7 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split_mfma(const AttnArg
   {
     const int span = (t0 + a.split_tokens - 1) / bs - b0 + 1;
     const int nb = span < a.max_blocks - b0 ? span : a.max_blocks - b0;
-    for (int i = tid; i < nb; i += kThreads)
+    for (int i = tid; i < nb; i += kMfmaThreads)
       s_blk[i] = a.tables[int64_t(r) * a.max_blocks + b0 + i];
   }
   const int T = clamp_len(a, a.seq_lens[r]);
@@ -738,7 +742,7 @@ __global__ __launch_bounds__(kThreads) void decode_attn_split_mfma(const AttnArg
     dst0[tid * head_stride + 1] = L;
   }
   __syncthreads();
-  for (int i = tid; i < kG * kDh; i += kThreads) {
+  for (int i = tid; i < kG * kDh; i += kMfmaThreads) {
     const int h = i / kDh, d = i % kDh;
     float A = 0.f;
 #pragma unroll
@@ -832,10 +836,12 @@ SplitFn pick_group(int G) {
   }
 }
 
+// 8 query heads per KV head at head_dim 128: the matrix-core pass (the
+// vector pass is near its ALU limit there)
+bool matrix_core_pass(int D, int G) { return D == 128 && G == 8; }
+
 SplitFn pick_split(int D, int G, bool lm) {
-  // 8 query heads per KV head at head_dim 128: the matrix-core pass (the
-  // vector pass is near its ALU limit there)
-  if (D == 128 && G == 8)
+  if (matrix_core_pass(D, G))
     return lm ? decode_attn_split_mfma<8, true> : decode_attn_split_mfma<8, false>;
   if (D == 64) return lm ? pick_group<64, true>(G) : pick_group<64, false>(G);
   return lm ? pick_group<128, true>(G) : pick_group<128, false>(G);
@@ -1072,7 +1078,8 @@ int launch_attention(const flowkv_pool* pool, int32_t layer, const void* q_dev, 
     SplitFn fn = pick_split(head_dim, G, lm);
     e = hipLaunchKernel(reinterpret_cast<const void*>(fn),
                         dim3(unsigned(kv_heads), unsigned(a.max_splits), unsigned(n_req)),
-                        dim3(kThreads), args, 0, st);
+                        dim3(matrix_core_pass(head_dim, G) ? kMfmaThreads : kVecThreads),
+                        args, 0, st);
   }
   if (e == hipSuccess) {
     const void* merge = head_dim == 64 ? reinterpret_cast<const void*>(decode_attn_merge<64>)
