@@ -305,9 +305,13 @@ def bench_attention(args):
     scale = 1.0 / geom.head_dim ** 0.5
     layer = geom.num_layers // 2
 
-    def step():
+    # the lengths travel on the host too, as a serving loop that keeps them
+    # there passes them (they then ride in the kernel arguments)
+    host_lens = lens if len(lens) <= fk.ATTN_INLINE_LENS else None
+
+    def step(host=True):
         fk.flowkv_decode_attention(pool, layer, q, tab_d, lens_d, max_seq, scale, out, ws,
-                                   args.split)
+                                   args.split, seq_lens_host=host_lens if host else None)
 
     for _ in range(args.warmup):
         step()
@@ -326,6 +330,23 @@ def bench_attention(args):
     ms = statistics.fmean(a.elapsed_time(b) for a, b in evs)
 
     context = {}
+    ab = None
+    if not args.no_context and host_lens is not None:
+        # the same step with the lengths in the kernel arguments and read from
+        # device memory, alternated step by step so that both see the same
+        # clocks and caches
+        evs_h, evs_d = timing_pairs(args.steps), timing_pairs(args.steps)
+        torch.cuda.synchronize()
+        for eh, ed in zip(evs_h, evs_d):
+            eh[0].record()
+            step(host=True)
+            eh[1].record()
+            ed[0].record()
+            step(host=False)
+            ed[1].record()
+        torch.cuda.synchronize()
+        ab = (statistics.median(a.elapsed_time(b) for a, b in evs_h),
+              statistics.median(a.elapsed_time(b) for a, b in evs_d))
     if not args.no_context:
         # plain contiguous device-to-device copy: context, and the kernel that
         # scales HBM counters taken from this process
@@ -341,9 +362,9 @@ def bench_attention(args):
             b_.copy_(a_)
         e1.record()
         torch.cuda.synchronize()
-        context = {"contiguous_copy_gbps": round(2 * nbytes / (e0.elapsed_time(e1) / 10 * 1e-3)
-                                                 / 1e9, 1),
-                   "contiguous_copy_bytes": nbytes}
+        context.update({"contiguous_copy_gbps": round(2 * nbytes / (e0.elapsed_time(e1) / 10
+                                                                     * 1e-3) / 1e9, 1),
+                        "contiguous_copy_bytes": nbytes})
         del a_, b_
 
     cpu = None
@@ -357,6 +378,12 @@ def bench_attention(args):
     ws_bytes = 2 * used_splits * q_heads * (geom.head_dim + 2) * 4
     algo = kv_bytes + q.numel() * 2 + out.numel() * 4 + ws_bytes + tab.nbytes
     achieved = algo / (ms * 1e-3) / 1e9
+    if ab is not None:
+        context["lengths_in_arguments_vs_device"] = {
+            "kernel_ms_median": [round(ab[0], 4), round(ab[1], 4)],
+            "roofline_frac": [round(algo / (x * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4) for x in ab],
+            "note": "the step with the lengths in the kernel arguments, then read from "
+                    "device memory, alternated step by step"}
     line = {
         "metric": "decode attention HBM GB/s (one layer, one token per request)",
         "value": round(achieved, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
@@ -367,7 +394,9 @@ def bench_attention(args):
                    "requests": len(lens), "tokens": int(lens.sum()), "q_heads": q_heads,
                    "kv_heads": geom.kv_heads, "head_dim": geom.head_dim,
                    "block_size": geom.block_size, "kv_dtype": "bf16",
-                   "layout": f"{args.layout}-major", "layer": layer, "split_tokens": split},
+                   "layout": f"{args.layout}-major", "layer": layer, "split_tokens": split,
+                   "lengths_in": ("kernel-arguments" if host_lens is not None
+                                  else "device-memory")},
         "kernel_ms_avg": round(ms, 4),
         "timing_events": TIMING["events"],
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,

@@ -315,6 +315,8 @@ int flowkv_transfer_layers(const flowkv_pool* src, const flowkv_pool* dst,
 #define FLOWKV_ATTN_MAX_SPLIT 1024     /* most tokens per pass-1 workgroup    */
 #define FLOWKV_ATTN_MIN_AUTO_SPLIT 256 /* least tokens the default rule picks */
 #define FLOWKV_ATTN_AUTO_PAIRS 512     /* (request, split) pairs it aims at   */
+#define FLOWKV_ATTN_INLINE_LENS 512    /* most host lengths a call carries in
+                                          the kernel arguments               */
 
 /* The split length used when split_tokens is 0: the smallest power of two s
    from FLOWKV_ATTN_MIN_AUTO_SPLIT to FLOWKV_ATTN_MAX_SPLIT with
@@ -339,7 +341,13 @@ int flowkv_decode_attention_workspace(int32_t n_req, int32_t q_heads, int32_t he
        out[r][h] = sum_t softmax_t(scale * q[r][h] . K[t][g]) * V[t][g]
    Token t lives in block block_tables[r * max_blocks + t / block_size], slot
    t % block_size.  Device inputs: q (n_req, q_heads, head_dim) bf16, 16-byte
-   aligned; block_tables (n_req, max_blocks) int32; seq_lens (n_req) int32.
+   aligned; block_tables (n_req, max_blocks) int32; seq_lens_dev (n_req)
+   int32.  seq_lens_host: the same lengths in host memory, or NULL.  When it
+   is given and n_req <= FLOWKV_ATTN_INLINE_LENS, the lengths travel in the
+   kernel arguments (copied at the call; the array may be reused as soon as
+   it returns) and seq_lens_dev is not read and may be NULL: a split past its
+   request's end then costs no memory access, which speeds up batches of
+   mixed lengths.  The two copies must agree; the host copy decides.
    Output: out (n_req, q_heads, head_dim) float32.  workspace: device memory
    of at least flowkv_decode_attention_workspace(...) bytes, owned by the
    caller, busy until the stream passes the call (NULL when that is 0).  Tokens beyond
@@ -355,9 +363,9 @@ int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer, const void* 
                             int32_t n_req, int32_t q_heads, int32_t kv_heads,
                             int32_t head_dim, const int32_t* block_tables_dev,
                             int32_t max_blocks, const int32_t* seq_lens_dev,
-                            int32_t max_seq_len, float scale, int32_t split_tokens,
-                            float* out_dev, void* workspace_dev, int64_t workspace_bytes,
-                            void* hip_stream);
+                            const int32_t* seq_lens_host, int32_t max_seq_len, float scale,
+                            int32_t split_tokens, float* out_dev, void* workspace_dev,
+                            int64_t workspace_bytes, void* hip_stream);
 
 /* For callers that cannot allocate device memory or pass a workspace: code
    under HIP graph capture, serving loops and harnesses that forbid
@@ -383,8 +391,9 @@ int flowkv_decode_attention_noalloc(const flowkv_pool* pool, int32_t layer, cons
                                     int32_t n_req, int32_t q_heads, int32_t kv_heads,
                                     int32_t head_dim, const int32_t* block_tables_dev,
                                     int32_t max_blocks, const int32_t* seq_lens_dev,
-                                    int32_t max_seq_len, float scale, int32_t split_tokens,
-                                    float* out_dev, void* hip_stream);
+                                    const int32_t* seq_lens_host, int32_t max_seq_len,
+                                    float scale, int32_t split_tokens, float* out_dev,
+                                    void* hip_stream);
 
 /* ---- load-aware scheduler (section 3.4; Appendix A, Algorithm 1) ------------
    Host only.  Each node reports a status vector S_i of 12 indicators, in

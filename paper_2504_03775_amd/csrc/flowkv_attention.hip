@@ -94,7 +94,13 @@ struct AttnArgs {
   int32_t layer, num_layers, block_size, kv_heads, q_heads, max_blocks;
   int32_t split_tokens, max_splits, max_seq_len;
   float scale_log2;                     // scale * log2(e)
+  // the requests' lengths, when the caller passed them on the host (the
+  // kernels instantiated with kLens read these instead of seq_lens)
+  int32_t lens[FLOWKV_ATTN_INLINE_LENS];
 };
+// The compiler appends 256 bytes of implicit arguments; the whole segment
+// stays within 4 KiB.
+static_assert(sizeof(AttnArgs) + 256 <= 4096, "kernel arguments must stay within 4 KiB");
 
 // Tokens of a request that take part: its length, capped by its block list
 // and by max_seq_len (which also bounds the workspace's split count).
@@ -104,9 +110,10 @@ __device__ __forceinline__ int clamp_len(const AttnArgs& a, int T) {
   return T < a.max_seq_len ? T : a.max_seq_len;
 }
 
-// A split at or past its request's end still leaves a record, an empty
-// partial (max -inf, sum 0) for each of its kG query heads, so that the merge
-// reads every split up to max_splits without the request's length.  Its
+// Without the lengths in the arguments, a split at or past its request's end
+// still leaves a record, an empty partial (max -inf, sum 0) for each of its
+// kG query heads, so that the merge reads every split up to max_splits
+// without the request's length.  Its
 // weighted-V part is never written; the merge ignores it.
 template <int kG, int kDh>
 __device__ __forceinline__ void write_empty_partial(const AttnArgs& a, int g, int split, int r,
@@ -161,7 +168,7 @@ template <> struct Words<2> {
   }
 };
 
-template <int kDh, int kG, bool kLM>
+template <int kDh, int kG, bool kLM, bool kLens>
 __global__ __launch_bounds__(kVecThreads) void decode_attn_split(const AttnArgs a) {
   constexpr int kW = kDh / 32;                  // bf16 pairs per lane (4 or 2)
   constexpr int kV = 2 * kW;                    // K/V values per lane
@@ -191,6 +198,10 @@ __global__ __launch_bounds__(kVecThreads) void decode_attn_split(const AttnArgs 
 
   const int t0 = split * a.split_tokens;
   const int bs = a.block_size;
+  // with the length in the arguments, a split past the request's end leaves
+  // at once, before any memory access, and writes no record
+  if constexpr (kLens)
+    if (t0 >= clamp_len(a, a.lens[r])) return;
   // the block IDs the split can touch, staged once in LDS: fetched without
   // waiting for the request's length (a split of at most
   // FLOWKV_ATTN_MAX_SPLIT tokens touches at most that many blocks plus one)
@@ -202,8 +213,8 @@ __global__ __launch_bounds__(kVecThreads) void decode_attn_split(const AttnArgs 
     for (int i = tid; i < nb; i += kVecThreads)
       s_blk[i] = a.tables[int64_t(r) * a.max_blocks + b0 + i];
   }
-  const int T = clamp_len(a, a.seq_lens[r]);
-  if (t0 >= T) {  // uniform: this split is past the request's end
+  const int T = clamp_len(a, kLens ? a.lens[r] : a.seq_lens[r]);
+  if (t0 >= T) {  // uniform: this split is past the request's end (no kLens)
     write_empty_partial<kG, kDh>(a, g, split, r, tid);
     return;
   }
@@ -468,7 +479,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 template <int kCtrl>
 __device__ __forceinline__ float dpp_max(float x) { return fmaxf(x, dpp<kCtrl>(x)); }
 
-template <int kG, bool kLM>
+template <int kG, bool kLM, bool kLens>
 __global__ __launch_bounds__(kMfmaThreads) void decode_attn_split_mfma(const AttnArgs a) {
   constexpr int kDh = 128;
   constexpr int kWaves = kMfmaThreads / 64;
@@ -492,6 +503,8 @@ __global__ __launch_bounds__(kMfmaThreads) void decode_attn_split_mfma(const Att
 
   const int t0 = split * a.split_tokens;
   const int bs = a.block_size;
+  if constexpr (kLens)
+    if (t0 >= clamp_len(a, a.lens[r])) return;
   __shared__ int32_t s_blk[FLOWKV_ATTN_MAX_SPLIT + 1];
   const int b0 = t0 / bs;
   {
@@ -500,8 +513,8 @@ __global__ __launch_bounds__(kMfmaThreads) void decode_attn_split_mfma(const Att
     for (int i = tid; i < nb; i += kMfmaThreads)
       s_blk[i] = a.tables[int64_t(r) * a.max_blocks + b0 + i];
   }
-  const int T = clamp_len(a, a.seq_lens[r]);
-  if (t0 >= T) {  // uniform: this split is past the request's end
+  const int T = clamp_len(a, kLens ? a.lens[r] : a.seq_lens[r]);
+  if (t0 >= T) {  // uniform: this split is past the request's end (no kLens)
     write_empty_partial<kG, kDh>(a, g, split, r, tid);
     return;
   }
@@ -761,14 +774,17 @@ __global__ __launch_bounds__(kMfmaThreads) void decode_attn_split_mfma(const Att
 constexpr int kMergeThreads = 256;
 constexpr int kMergeChunk = 16;
 
-template <int kDh>
+template <int kDh, bool kLens>
 __global__ __launch_bounds__(kMergeThreads) void decode_attn_merge(const AttnArgs a) {
   constexpr int kParts = kMergeThreads / kDh;
   const int h = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
   const int d = tid % kDh, part = tid / kDh;
-  const int ns = a.max_splits;
+  // records per (request, head); with the lengths in the arguments only the
+  // request's own splits hold one
+  int ns = a.max_splits;
+  if constexpr (kLens) ns = (clamp_len(a, a.lens[r]) + a.split_tokens - 1) / a.split_tokens;
   float* o = a.out + (int64_t(r) * a.q_heads + h) * kDh;
-  const float* src = a.ws + (int64_t(r) * a.q_heads + h) * ns * (kDh + 2);
+  const float* src = a.ws + (int64_t(r) * a.q_heads + h) * a.max_splits * (kDh + 2);
   float m = -INFINITY, l = 0.f, acc = 0.f;
   for (int x0 = part; x0 < ns; x0 += kParts * kMergeChunk) {
     // branch-free loads: a split past the end re-reads split 0 and is
@@ -826,13 +842,13 @@ __global__ __launch_bounds__(kMergeThreads) void decode_attn_merge(const AttnArg
 
 using SplitFn = void (*)(AttnArgs);
 
-template <int D, bool LM>
+template <int D, bool LM, bool L>
 SplitFn pick_group(int G) {
   switch (G) {
-    case 1: return decode_attn_split<D, 1, LM>;
-    case 2: return decode_attn_split<D, 2, LM>;
-    case 4: return decode_attn_split<D, 4, LM>;
-    default: return decode_attn_split<D, 8, LM>;
+    case 1: return decode_attn_split<D, 1, LM, L>;
+    case 2: return decode_attn_split<D, 2, LM, L>;
+    case 4: return decode_attn_split<D, 4, LM, L>;
+    default: return decode_attn_split<D, 8, LM, L>;
   }
 }
 
@@ -840,11 +856,24 @@ SplitFn pick_group(int G) {
 // vector pass is near its ALU limit there)
 bool matrix_core_pass(int D, int G) { return D == 128 && G == 8; }
 
-SplitFn pick_split(int D, int G, bool lm) {
+template <bool L>
+SplitFn pick_split_lens(int D, int G, bool lm) {
   if (matrix_core_pass(D, G))
-    return lm ? decode_attn_split_mfma<8, true> : decode_attn_split_mfma<8, false>;
-  if (D == 64) return lm ? pick_group<64, true>(G) : pick_group<64, false>(G);
-  return lm ? pick_group<128, true>(G) : pick_group<128, false>(G);
+    return lm ? decode_attn_split_mfma<8, true, L> : decode_attn_split_mfma<8, false, L>;
+  if (D == 64) return lm ? pick_group<64, true, L>(G) : pick_group<64, false, L>(G);
+  return lm ? pick_group<128, true, L>(G) : pick_group<128, false, L>(G);
+}
+
+SplitFn pick_split(int D, int G, bool lm, bool lens) {
+  return lens ? pick_split_lens<true>(D, G, lm) : pick_split_lens<false>(D, G, lm);
+}
+
+const void* pick_merge(int D, bool lens) {
+  if (D == 64)
+    return lens ? reinterpret_cast<const void*>(decode_attn_merge<64, true>)
+                : reinterpret_cast<const void*>(decode_attn_merge<64, false>);
+  return lens ? reinterpret_cast<const void*>(decode_attn_merge<128, true>)
+              : reinterpret_cast<const void*>(decode_attn_merge<128, false>);
 }
 
 int32_t auto_split(int32_t n_req, int32_t max_seq_len) {
@@ -892,9 +921,9 @@ namespace {
 int launch_attention(const flowkv_pool* pool, int32_t layer, const void* q_dev, int32_t n_req,
                      int32_t q_heads, int32_t kv_heads, int32_t head_dim,
                      const int32_t* block_tables_dev, int32_t max_blocks,
-                     const int32_t* seq_lens_dev, int32_t max_seq_len, float scale,
-                     int32_t split_tokens, float* out_dev, void* ws, int64_t ws_cap,
-                     bool scratch_ws, void* hip_stream);
+                     const int32_t* seq_lens_dev, const int32_t* seq_lens_host,
+                     int32_t max_seq_len, float scale, int32_t split_tokens, float* out_dev,
+                     void* ws, int64_t ws_cap, bool scratch_ws, void* hip_stream);
 
 }  // namespace
 
@@ -902,14 +931,15 @@ extern "C" int flowkv_decode_attention(const flowkv_pool* pool, int32_t layer,
                                        const void* q_dev, int32_t n_req, int32_t q_heads,
                                        int32_t kv_heads, int32_t head_dim,
                                        const int32_t* block_tables_dev, int32_t max_blocks,
-                                       const int32_t* seq_lens_dev, int32_t max_seq_len,
+                                       const int32_t* seq_lens_dev,
+                                       const int32_t* seq_lens_host, int32_t max_seq_len,
                                        float scale, int32_t split_tokens, float* out_dev,
                                        void* workspace_dev, int64_t workspace_bytes,
                                        void* hip_stream) {
   return launch_attention(pool, layer, q_dev, n_req, q_heads, kv_heads, head_dim,
-                          block_tables_dev, max_blocks, seq_lens_dev, max_seq_len, scale,
-                          split_tokens, out_dev, workspace_dev, workspace_bytes, false,
-                          hip_stream);
+                          block_tables_dev, max_blocks, seq_lens_dev, seq_lens_host,
+                          max_seq_len, scale, split_tokens, out_dev, workspace_dev,
+                          workspace_bytes, false, hip_stream);
 }
 
 // ---- the variant that allocates nothing --------------------------------------
@@ -964,13 +994,14 @@ extern "C" int flowkv_decode_attention_noalloc(const flowkv_pool* pool, int32_t 
                                                int32_t head_dim,
                                                const int32_t* block_tables_dev,
                                                int32_t max_blocks, const int32_t* seq_lens_dev,
+                                               const int32_t* seq_lens_host,
                                                int32_t max_seq_len, float scale,
                                                int32_t split_tokens, float* out_dev,
                                                void* hip_stream) {
   return launch_attention(pool, layer, q_dev, n_req, q_heads, kv_heads, head_dim,
-                          block_tables_dev, max_blocks, seq_lens_dev, max_seq_len, scale,
-                          split_tokens, out_dev, nullptr, FLOWKV_ATTN_SCRATCH_BYTES, true,
-                          hip_stream);
+                          block_tables_dev, max_blocks, seq_lens_dev, seq_lens_host,
+                          max_seq_len, scale, split_tokens, out_dev, nullptr,
+                          FLOWKV_ATTN_SCRATCH_BYTES, true, hip_stream);
 }
 
 namespace {
@@ -978,9 +1009,10 @@ namespace {
 int launch_attention(const flowkv_pool* pool, int32_t layer, const void* q_dev, int32_t n_req,
                      int32_t q_heads, int32_t kv_heads, int32_t head_dim,
                      const int32_t* block_tables_dev, int32_t max_blocks,
-                     const int32_t* seq_lens_dev, int32_t max_seq_len, float scale,
-                     int32_t split_tokens, float* out_dev, void* workspace_dev,
-                     int64_t workspace_bytes, bool scratch_ws, void* hip_stream) {
+                     const int32_t* seq_lens_dev, const int32_t* seq_lens_host,
+                     int32_t max_seq_len, float scale, int32_t split_tokens, float* out_dev,
+                     void* workspace_dev, int64_t workspace_bytes, bool scratch_ws,
+                     void* hip_stream) {
   if (!pool) return fail(FLOWKV_EINVAL, "NULL pool");
   if (pool->layout != FLOWKV_LAYOUT_LAYER_MAJOR && pool->layout != FLOWKV_LAYOUT_BLOCK_MAJOR)
     return fail(FLOWKV_EINVAL, "unknown layout %d", pool->layout);
@@ -1022,7 +1054,10 @@ int launch_attention(const flowkv_pool* pool, int32_t layer, const void* q_dev, 
   if (n_req == 0) return ok();
   const int64_t need = ws_bytes(n_req, q_heads, head_dim, max_seq_len, split_tokens);
   // (a workspace of 0 bytes, when max_seq_len is 0, may be NULL)
-  if (!q_dev || !block_tables_dev || !seq_lens_dev || !out_dev ||
+  // lengths from the host ride in the kernel arguments (then the device
+  // copy is not read)
+  const bool lens = seq_lens_host && n_req <= FLOWKV_ATTN_INLINE_LENS;
+  if (!q_dev || !block_tables_dev || (!seq_lens_dev && !lens) || !out_dev ||
       (!scratch_ws && !workspace_dev && need > 0))
     return fail(FLOWKV_EINVAL, "NULL device pointer");
   if (workspace_bytes < need) {
@@ -1071,21 +1106,21 @@ int launch_attention(const flowkv_pool* pool, int32_t layer, const void* q_dev, 
   a.max_splits = int32_t((int64_t(max_seq_len) + split_tokens - 1) / split_tokens);
   a.max_seq_len = max_seq_len;
   a.scale_log2 = scale * kLog2e;
+  if (lens)
+    for (int32_t i = 0; i < n_req; ++i) a.lens[i] = seq_lens_host[i];
   hipStream_t st = static_cast<hipStream_t>(hip_stream);
   void* args[] = {&a};
   hipError_t e = hipSuccess;
   if (a.max_splits > 0) {
-    SplitFn fn = pick_split(head_dim, G, lm);
+    SplitFn fn = pick_split(head_dim, G, lm, lens);
     e = hipLaunchKernel(reinterpret_cast<const void*>(fn),
                         dim3(unsigned(kv_heads), unsigned(a.max_splits), unsigned(n_req)),
                         dim3(matrix_core_pass(head_dim, G) ? kMfmaThreads : kVecThreads),
                         args, 0, st);
   }
   if (e == hipSuccess) {
-    const void* merge = head_dim == 64 ? reinterpret_cast<const void*>(decode_attn_merge<64>)
-                                       : reinterpret_cast<const void*>(decode_attn_merge<128>);
-    e = hipLaunchKernel(merge, dim3(unsigned(q_heads), unsigned(n_req)), dim3(kMergeThreads),
-                        args, 0, st);
+    e = hipLaunchKernel(pick_merge(head_dim, lens), dim3(unsigned(q_heads), unsigned(n_req)),
+                        dim3(kMergeThreads), args, 0, st);
   }
   if (e == hipSuccess) e = hipGetLastError();
   if (e != hipSuccess) return fail(FLOWKV_EHIP, "attention launch: %s", hipGetErrorString(e));

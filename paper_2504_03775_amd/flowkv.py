@@ -122,14 +122,16 @@ SIGNATURES = {
     "flowkv_decode_attention": (ctypes.c_int, [_POOLP, ctypes.c_int32, ctypes.c_void_p,
                                                ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                                ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
-                                               ctypes.c_void_p, ctypes.c_int32, ctypes.c_float,
+                                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                               ctypes.c_float,
                                                ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                                ctypes.c_int64, ctypes.c_void_p]),
     "flowkv_decode_attention_noalloc": (ctypes.c_int, [_POOLP, ctypes.c_int32, ctypes.c_void_p,
                                                        ctypes.c_int32, ctypes.c_int32,
                                                        ctypes.c_int32, ctypes.c_int32,
                                                        ctypes.c_void_p, ctypes.c_int32,
-                                                       ctypes.c_void_p, ctypes.c_int32,
+                                                       ctypes.c_void_p, ctypes.c_void_p,
+                                                       ctypes.c_int32,
                                                        ctypes.c_float, ctypes.c_int32,
                                                        ctypes.c_void_p, ctypes.c_void_p]),
     "flowkv_sched_create": (ctypes.c_int, [ctypes.POINTER(flowkv_sched_params), ctypes.c_int32,
@@ -558,6 +560,18 @@ def flowkv_decode_attention_workspace(n_req: int, q_heads: int, head_dim: int,
 
 
 ATTN_SCRATCH_BYTES = 16 << 20  # scratch of flowkv_decode_attention_noalloc, per GPU
+ATTN_INLINE_LENS = 512  # most host lengths a call carries in the kernel arguments
+
+
+def _host_lens(seq_lens_host, n):
+    """The host copy of the lengths as a contiguous int32 array (kept alive by
+    the caller for the duration of the call), or None."""
+    if seq_lens_host is None:
+        return None
+    h = np.ascontiguousarray(seq_lens_host, dtype=np.int32)
+    if h.shape != (n,):
+        raise ValueError("seq_lens_host: need one length per request")
+    return h
 
 
 def _check_attention_tensors(pool: KVPool, q, block_tables, seq_lens, out):
@@ -575,32 +589,39 @@ def _check_attention_tensors(pool: KVPool, q, block_tables, seq_lens, out):
 
 def flowkv_decode_attention_noalloc(pool: KVPool, layer: int, q, block_tables, seq_lens,
                                     max_seq_len: int, scale: float, out,
-                                    split_tokens: int = 0, stream=None) -> None:
+                                    split_tokens: int = 0, stream=None,
+                                    seq_lens_host=None) -> None:
     """flowkv_decode_attention without a workspace argument: the partial
     results go to the library's fixed per-GPU scratch (ATTN_SCRATCH_BYTES);
     calls that overlap on one GPU race."""
     n, hq, dh = _check_attention_tensors(pool, q, block_tables, seq_lens, out)
+    hl = _host_lens(seq_lens_host, n)
     _check(_lib.flowkv_decode_attention_noalloc(
         ctypes.byref(pool.desc), layer, ctypes.c_void_p(q.data_ptr()), n, hq, pool.kv_heads, dh,
         ctypes.c_void_p(block_tables.data_ptr()), block_tables.shape[1],
-        ctypes.c_void_p(seq_lens.data_ptr()), max_seq_len, scale, split_tokens,
+        ctypes.c_void_p(seq_lens.data_ptr()), _ptr(hl) if hl is not None else None,
+        max_seq_len, scale, split_tokens,
         ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(_stream_handle(stream))),
         "flowkv_decode_attention_noalloc")
 
 
 def flowkv_decode_attention(pool: KVPool, layer: int, q, block_tables, seq_lens,
                             max_seq_len: int, scale: float, out, workspace,
-                            split_tokens: int = 0, stream=None) -> None:
+                            split_tokens: int = 0, stream=None, seq_lens_host=None) -> None:
     """Decode attention of layer `layer` over `pool` (torch device tensors:
     q (n, Hq, Dh) bf16, block_tables (n, max_blocks) int32, seq_lens (n,)
-    int32, out (n, Hq, Dh) float32, workspace uint8)."""
+    int32, out (n, Hq, Dh) float32, workspace uint8).  seq_lens_host, an
+    optional host copy of the lengths (int32-convertible, one per request),
+    lets the call carry them in the kernel arguments (ATTN_INLINE_LENS)."""
     n, hq, dh = _check_attention_tensors(pool, q, block_tables, seq_lens, out)
     if not workspace.is_contiguous() or workspace.device != pool.device:
         raise ValueError("attention workspace: not a contiguous tensor on the pool's device")
+    hl = _host_lens(seq_lens_host, n)
     _check(_lib.flowkv_decode_attention(
         ctypes.byref(pool.desc), layer, ctypes.c_void_p(q.data_ptr()), n, hq, pool.kv_heads, dh,
         ctypes.c_void_p(block_tables.data_ptr()), block_tables.shape[1],
-        ctypes.c_void_p(seq_lens.data_ptr()), max_seq_len, scale, split_tokens,
+        ctypes.c_void_p(seq_lens.data_ptr()), _ptr(hl) if hl is not None else None,
+        max_seq_len, scale, split_tokens,
         ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(workspace.data_ptr()),
         workspace.numel() * workspace.element_size(), ctypes.c_void_p(_stream_handle(stream))),
         "flowkv_decode_attention")

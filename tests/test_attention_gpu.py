@@ -38,7 +38,7 @@ def bf16_to_f64(t: torch.Tensor) -> np.ndarray:
 
 
 def run_case(geom: Geometry, layout, pool_blocks, lens, q_heads, seed, split=0, layer=None,
-             max_seq=None, check=True):
+             max_seq=None, check=True, host_lens=False):
     g = np.random.default_rng(seed)
     layer = int(g.integers(geom.num_layers)) if layer is None else layer
     pool = fk.KVPool(layout, make_device_pool(geom, layout, pool_blocks, "cuda", seed))
@@ -64,7 +64,8 @@ def run_case(geom: Geometry, layout, pool_blocks, lens, q_heads, seed, split=0, 
     scale = 1.0 / np.sqrt(geom.head_dim)
     fk.flowkv_decode_attention(pool, layer, q, torch.as_tensor(tab, device="cuda"),
                                torch.as_tensor(np.asarray(lens, np.int32), device="cuda"),
-                               max_seq, scale, out, ws, split)
+                               max_seq, scale, out, ws, split,
+                               seq_lens_host=np.asarray(lens, np.int32) if host_lens else None)
     torch.cuda.synchronize()
     got = out.cpu().numpy().astype(np.float64)
     if not check:
@@ -165,6 +166,44 @@ def test_both_layouts_give_identical_outputs():
         torch.cuda.synchronize()
         outs.append(out.cpu())
     assert torch.equal(outs[0], outs[1])
+
+
+HOST_LENS_SHAPES = [  # (layers, kv heads, head dim, block size, q heads): every pass
+    (2, 2, 64, 16, 2), (2, 2, 64, 16, 4), (2, 1, 64, 16, 8), (2, 4, 128, 16, 4),
+    (2, 2, 128, 16, 16), (2, 1, 128, 7, 1), (2, 2, 128, 16, 4),
+]
+
+
+@pytest.mark.parametrize("shape", range(len(HOST_LENS_SHAPES)))
+@pytest.mark.parametrize("layout", [BM, LM], ids=lambda x: NAMES[x])
+def test_host_lengths_give_identical_outputs(layout, shape):
+    """Lengths passed on the host travel in the kernel arguments: splits past
+    a request's end then leave no record and the merge reads only the live
+    ones.  The arithmetic is the same, so the outputs are bit-identical to the
+    device-lengths call, for every pass (vector at 1, 2, 4 and 8 query heads
+    per KV head, both head dims; matrix-core at 8 over head_dim 128), mixed
+    lengths with empty requests, lengths past max_seq_len and past the block
+    table; and they pass the oracle."""
+    L, hkv, dh, bs, hq = HOST_LENS_SHAPES[shape]
+    geom = Geometry(f"hl{shape}", L, hkv, dh, bs, "bfloat16")
+    g = np.random.default_rng(700 + shape)
+    lens = [int(x) for x in g.integers(1, 900, size=5)] + [0, 1, 1500]
+    split = [0, 64, 128, 300][shape % 4]
+    max_seq = 1200          # the 1,500-token request is cut at 1,200 tokens
+    blocks = sum(max(1, -(-T // bs)) for T in lens) + 8
+    say(f"host lengths {NAMES[layout]} L={L} Hkv={hkv} Hq={hq} Dh={dh} bs={bs} lens={lens} "
+        f"split={split}")
+    dev_out, _ = run_case(geom, layout, blocks, lens, hq, 40 + shape, split, max_seq=max_seq,
+                          check=False)
+    host_out, _ = run_case(geom, layout, blocks, lens, hq, 40 + shape, split, max_seq=max_seq,
+                           check=False, host_lens=True)
+    assert np.array_equal(dev_out, host_out, equal_nan=False)
+    assert np.all(host_out[5] == 0)          # the empty request
+    # the oracle takes no empty request: the same lengths without it
+    live = lens[:5] + lens[6:]
+    _, err = run_case(geom, layout, blocks, live, hq, 40 + shape, split, max_seq=max_seq,
+                      host_lens=True)
+    say(f"  identical to the device-lengths call; max error {err:.2e}")
 
 
 def test_length_caps_and_empty_request():
@@ -279,9 +318,11 @@ def test_bench_attention_workloads_full_size(name, layout):
     """Each --op attention workload exactly as bench.py runs it: its recipe's
     block lists, the full receiver pool (block-major, and for the batch also
     layer-major as --layout layer runs it; seeded N(0,1)), every request in
-    one call, the default split, the middle layer; the outputs of a sample
-    of requests (shortest, longest and two between) against the oracle on
-    just those requests' blocks of that layer."""
+    one call with the lengths on the host, the default split, the middle
+    layer; the outputs of a sample of requests (shortest, longest and two
+    between) against the oracle on just those requests' blocks of that
+    layer, and every output against the same call with the lengths read on
+    the device."""
     make, q_heads = BENCH_ATTN[name]
     wl = make(lambda P, pol, seed: fk.Allocator(P, pol, seed))
     geom = wl.geom
@@ -301,8 +342,16 @@ def test_bench_attention_workloads_full_size(name, layout):
                      dtype=torch.uint8, device="cuda")
     out = torch.full((n, q_heads, geom.head_dim), float("nan"), dtype=torch.float32, device="cuda")
     fk.flowkv_decode_attention(pool, layer, q, torch.as_tensor(tab, device="cuda"),
-                               torch.as_tensor(lens, device="cuda"), max_seq, scale, out, ws)
+                               torch.as_tensor(lens, device="cuda"), max_seq, scale, out, ws,
+                               seq_lens_host=lens)
     torch.cuda.synchronize()
+    # the same call with the lengths read on the device: bit-identical
+    out_dev = torch.empty_like(out)
+    fk.flowkv_decode_attention(pool, layer, q, torch.as_tensor(tab, device="cuda"),
+                               torch.as_tensor(lens, device="cuda"), max_seq, scale, out_dev, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(out, out_dev)
+    del out_dev
     order = np.argsort(lens, kind="stable")
     pick = sorted({int(order[0]), int(order[-1]), int(order[n // 3]), int(order[(2 * n) // 3])})
     say(f"{name}: {n} requests, {int(lens.sum())} tokens, pool {wl.dst_pool_blocks} blocks, "

@@ -58,9 +58,10 @@ def metadata(asm, name):
     return m.group(1)
 
 
+@pytest.mark.parametrize("lens", ["Lb0", "Lb1"], ids=["lengths-on-device", "lengths-in-arguments"])
 @pytest.mark.parametrize("layout", ["Lb0", "Lb1"], ids=["block-major", "layer-major"])
-def test_mfma_wait_matches_the_loads_the_loop_issues(asm, layout):
-    name, body = kernel_text(asm, rf"_ZN\w*decode_attn_split_mfmaILi8E{layout}EEEvN\w+")
+def test_mfma_wait_matches_the_loads_the_loop_issues(asm, layout, lens):
+    name, body = kernel_text(asm, rf"_ZN\w*decode_attn_split_mfmaILi8E{layout}E{lens}EEEvN\w+")
     waits = [int(x) for x in re.findall(r"s_waitcnt vmcnt\((\d+)\)", body)]
     explicit = [w for w in waits if w > 0]
     assert len(explicit) == 1, waits

@@ -73,6 +73,7 @@ def test_binding_constants_match_the_header():
     assert int(defines["FLOWKV_INLINE_LAYERS"]) == fk.INLINE_LAYERS
     assert int(defines["FLOWKV_INLINE_RUNS_LAYER_MAJOR"]) == fk.INLINE_RUNS_LAYER_MAJOR
     assert int(defines["FLOWKV_ATTN_SCRATCH_BYTES"]) == fk.ATTN_SCRATCH_BYTES
+    assert int(defines["FLOWKV_ATTN_INLINE_LENS"]) == fk.ATTN_INLINE_LENS
     enums = dict(re.findall(r"\b(FLOWKV_E?\w+)\s*=\s*(-?\d+)", text))
     for name in ("OK", "EINVAL", "ENOSPC", "ERANGE", "EDUP", "ECAP", "EHIP", "ENOMEM"):
         assert int(enums["FLOWKV_" + name]) == getattr(fk, name), name
@@ -706,11 +707,12 @@ def test_binding_shares_torchs_hip_runtime():
 # ---- decode attention argument checks (rejected before any device call) ------
 
 def attn(p, layer=0, q=1 << 12, n_req=1, hq=8, hkv=2, dh=128, tables=1 << 16, max_blocks=4,
-         lens=1 << 18, max_seq=64, scale=0.1, split=0, out=1 << 20, ws=1 << 24, ws_bytes=1 << 30):
+         lens=1 << 18, max_seq=64, scale=0.1, split=0, out=1 << 20, ws=1 << 24, ws_bytes=1 << 30,
+         host_lens=None):
     return fk.lib().flowkv_decode_attention(
         ctypes.byref(p), layer, ctypes.c_void_p(q), n_req, hq, hkv, dh, ctypes.c_void_p(tables),
-        max_blocks, ctypes.c_void_p(lens), max_seq, scale, split, ctypes.c_void_p(out),
-        ctypes.c_void_p(ws), ws_bytes, None)
+        max_blocks, ctypes.c_void_p(lens), host_lens, max_seq, scale, split,
+        ctypes.c_void_p(out), ctypes.c_void_p(ws), ws_bytes, None)
 
 
 def test_attention_rejects_bad_arguments_without_touching_the_device():
@@ -732,13 +734,23 @@ def test_attention_rejects_bad_arguments_without_touching_the_device():
     assert attn(pool(L=2, B=8, chunk=chunk + 16)) == fk.EINVAL    # chunk not bs x Hkv x Dh x 2
     assert attn(pool(layout=7, L=2, B=8, chunk=chunk)) == fk.EINVAL
     assert attn(pool(L=2, B=8, chunk=chunk, bases=(0,))) == fk.EINVAL   # NULL base
+    # the device lengths may be NULL only when the host copy travels in the
+    # kernel arguments (at most ATTN_INLINE_LENS requests)
+    assert attn(p, lens=0) == fk.EINVAL
+    big = np.zeros(fk.ATTN_INLINE_LENS + 1, np.int32)
+    assert attn(p, lens=0, n_req=len(big), host_lens=big.ctypes.data, ws_bytes=16) == fk.EINVAL
+    assert attn(p, n_req=len(big), host_lens=big.ctypes.data, ws_bytes=16) == fk.ECAP
+    ok = np.zeros(fk.ATTN_INLINE_LENS, np.int32)
+    assert attn(p, lens=0, n_req=len(ok), host_lens=ok.ctypes.data, ws_bytes=16) == fk.ECAP
 
 
 def attn_noalloc(p, layer=0, q=1 << 12, n_req=1, hq=8, hkv=2, dh=128, tables=1 << 16,
-                 max_blocks=4, lens=1 << 18, max_seq=64, scale=0.1, split=0, out=1 << 20):
+                 max_blocks=4, lens=1 << 18, max_seq=64, scale=0.1, split=0, out=1 << 20,
+                 host_lens=None):
     return fk.lib().flowkv_decode_attention_noalloc(
         ctypes.byref(p), layer, ctypes.c_void_p(q), n_req, hq, hkv, dh, ctypes.c_void_p(tables),
-        max_blocks, ctypes.c_void_p(lens), max_seq, scale, split, ctypes.c_void_p(out), None)
+        max_blocks, ctypes.c_void_p(lens), host_lens, max_seq, scale, split,
+        ctypes.c_void_p(out), None)
 
 
 def test_noalloc_attention_rejects_before_any_runtime_call():
@@ -751,7 +763,8 @@ def test_noalloc_attention_rejects_before_any_runtime_call():
     assert fk.ATTN_SCRATCH_BYTES == 16 << 20
     assert attn_noalloc(p, n_req=0) == fk.OK
     for c in (dict(layer=2), dict(dh=96), dict(hq=6, hkv=4), dict(split=1025), dict(scale=0.0),
-              dict(q=(1 << 12) + 8), dict(q=0), dict(out=0), dict(max_blocks=-1)):
+              dict(q=(1 << 12) + 8), dict(q=0), dict(out=0), dict(max_blocks=-1),
+              dict(lens=0)):
         assert attn_noalloc(p, **c) == fk.EINVAL, c
     # the need is n_req x q_heads x splits x (head_dim + 2) floats: find the
     # largest request count that fits the scratch at 32 query heads over 8

@@ -50,9 +50,14 @@ def both(geom, args, scale, layer):
                      dtype=torch.uint8, device="cuda")
     want = torch.full((n, hq, dh), float("nan"), dtype=torch.float32, device="cuda")
     got = torch.full_like(want, float("nan"))
+    got_host = torch.full_like(want, float("nan"))
     fk.flowkv_decode_attention(pool, layer, q, tab, sl, max_seq, scale, want, ws, split)
     fk.flowkv_decode_attention_noalloc(pool, layer, q, tab, sl, max_seq, scale, got, split)
+    # and with the lengths on the host (carried in the kernel arguments)
+    fk.flowkv_decode_attention_noalloc(pool, layer, q, tab, sl, max_seq, scale, got_host, split,
+                                       seq_lens_host=sl.cpu().numpy())
     torch.cuda.synchronize()
+    assert torch.equal(got.cpu(), got_host.cpu()), "host-lengths call differs"
     return want.cpu(), got.cpu()
 
 
