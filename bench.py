@@ -345,8 +345,8 @@ def bench_attention(args):
             step(host=False)
             ed[1].record()
         torch.cuda.synchronize()
-        ab = (statistics.median(a.elapsed_time(b) for a, b in evs_h),
-              statistics.median(a.elapsed_time(b) for a, b in evs_d))
+        ab = (statistics.fmean(a.elapsed_time(b) for a, b in evs_h),
+              statistics.fmean(a.elapsed_time(b) for a, b in evs_d))
     if not args.no_context:
         # plain contiguous device-to-device copy: context, and the kernel that
         # scales HBM counters taken from this process
@@ -380,7 +380,7 @@ def bench_attention(args):
     achieved = algo / (ms * 1e-3) / 1e9
     if ab is not None:
         context["lengths_in_arguments_vs_device"] = {
-            "kernel_ms_median": [round(ab[0], 4), round(ab[1], 4)],
+            "kernel_ms_avg": [round(ab[0], 4), round(ab[1], 4)],
             "roofline_frac": [round(algo / (x * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4) for x in ab],
             "note": "the step with the lengths in the kernel arguments, then read from "
                     "device memory, alternated step by step"}
