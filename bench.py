@@ -398,6 +398,8 @@ def bench_attention(args):
                    "lengths_in": ("kernel-arguments" if host_lens is not None
                                   else "device-memory")},
         "kernel_ms_avg": round(ms, 4),
+        "kernel_ms_p10_p50_p90": [round(float(x), 4) for x in
+                                  np.percentile([a.elapsed_time(b) for a, b in evs], [10, 50, 90])],
         "timing_events": TIMING["events"],
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
