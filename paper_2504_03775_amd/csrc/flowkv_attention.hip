@@ -39,6 +39,12 @@
 //           (reference max, sum, weighted V) per query head.
 //   pass 2: one workgroup per (query head, request) merges the splits,
 //           several splits per thread in flight.
+// The grid covers every split up to the longest request.  When the caller
+// passes the lengths on the host they ride in the kernel arguments (the
+// kLens instantiations): a split past its request's end then leaves before
+// any memory access and writes nothing, and pass 2 reads only the
+// request's own splits.  Otherwise the lengths come from device memory and
+// such a split leaves an empty record for pass 2.
 // All arithmetic is float32; exponentials are exp2 of scores scaled by
 // log2(e).  K and V are bfloat16; the output is float32.
 #include <hip/hip_runtime.h>
@@ -113,8 +119,8 @@ __device__ __forceinline__ int clamp_len(const AttnArgs& a, int T) {
 // Without the lengths in the arguments, a split at or past its request's end
 // still leaves a record, an empty partial (max -inf, sum 0) for each of its
 // kG query heads, so that the merge reads every split up to max_splits
-// without the request's length.  Its
-// weighted-V part is never written; the merge ignores it.
+// without the request's length.  Its weighted-V part is never written; the
+// merge ignores it.
 template <int kG, int kDh>
 __device__ __forceinline__ void write_empty_partial(const AttnArgs& a, int g, int split, int r,
                                                     int tid) {
@@ -765,12 +771,13 @@ __global__ __launch_bounds__(kMfmaThreads) void decode_attn_split_mfma(const Att
 }
 
 // Pass 2: one workgroup per (query head, request).  Every split up to
-// max_splits has a record (pass 1 leaves an empty one past a request's end),
-// so the merge needs no request length and no chain of dependent loads: a
-// thread set of Dh threads takes every (256 / Dh)-th split, kMergeChunk
-// splits' records loaded at once (all of them in one round for up to
-// 256 / Dh x kMergeChunk splits), folded into a running (max, sum, weighted V)
-// that is rescaled when its max rises; the sets then meet in LDS.
+// max_splits has a record (pass 1 leaves an empty one past a request's end;
+// with kLens the merge reads only the request's own splits instead), so the
+// merge needs no chain of dependent loads: a thread set of Dh threads takes
+// every (256 / Dh)-th split, kMergeChunk splits' records loaded at once (all
+// of them in one round for up to 256 / Dh x kMergeChunk splits), folded into
+// a running (max, sum, weighted V) that is rescaled when its max rises; the
+// sets then meet in LDS.
 constexpr int kMergeThreads = 256;
 constexpr int kMergeChunk = 16;
 
