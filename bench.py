@@ -750,7 +750,9 @@ def bench_table3(args):
     seeded free list of the 30%-occupied pool), in two forms:
       one_launch  the whole plan in one launch (plan in the kernel arguments
                   when it fits there, else staged);
-      layerwise   32 launches, one per layer (K and V of that layer).
+      layerwise   32 launches, one per layer (K and V of that layer);
+    and, by kernel time only, the layerwise launches replayed from a HIP
+    graph captured once (layerwise_graph).
     Per form and length: the median kernel time (HIP events around the
     launches), the step time back to back, and the synchronised request
     latency (plan, staging, launches and kernels, synchronised; median of
@@ -838,6 +840,31 @@ def bench_table3(args):
         row["layerwise_over_one_launch"] = {
             k: round(row["layerwise"][k] / row["one_launch"][k], 2)
             for k in ("kernel_ms_median", "ms_per_step", "latency_ms_median")}
+        # the same 32 per-layer launches captured once in a HIP graph and
+        # replayed: what the gaps between dispatches cost.  The plan is fixed
+        # at capture, so only the kernel time compares.
+        segs = fk.flowkv_plan(S, D, src.num_blocks, dst.num_blocks)
+        segs_g = fk.segments_to_device(segs, dev)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for layer in range(geom.num_layers):
+                fk.flowkv_transfer_layers(src, dst, segs_g, len(segs), n, layer, 1)
+        for _ in range(max(1, args.warmup)):
+            graph.replay()
+        evs = timing_pairs(args.steps)
+        torch.cuda.synchronize()
+        for e in evs:
+            e[0].record(stream)
+            graph.replay()
+            e[1].record(stream)
+        torch.cuda.synchronize()
+        k_g = statistics.median(a.elapsed_time(b) for a, b in evs)
+        row["layerwise_graph"] = {"kernel_ms_median": round(k_g, 4),
+                                  "launches": geom.num_layers,
+                                  "over_one_launch": round(
+                                      k_g / row["one_launch"]["kernel_ms_median"], 2)}
+        del graph, segs_g
         if T in TABLE3_PAPER_S:
             row["paper_s_single_l20"] = dict(zip(("flowkv", "flowkv_layerwise"),
                                                  TABLE3_PAPER_S[T]))

@@ -198,6 +198,7 @@ def test_table3_line_contract():
     for r in j["rows"]:
         assert r["blocks"] == -(-r["tokens"] // 16)
         assert r["one_launch"]["launches"] == 1 and r["layerwise"]["launches"] == 32
+        assert r["layerwise_graph"]["launches"] == 32 and r["layerwise_graph"]["kernel_ms_median"] > 0
         for form in ("one_launch", "layerwise"):
             assert all(r[form][k] > 0 for k in ("kernel_ms_median", "ms_per_step",
                                                  "latency_ms_median"))
