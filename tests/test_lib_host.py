@@ -744,6 +744,19 @@ def test_attention_rejects_bad_arguments_without_touching_the_device():
     assert attn(p, lens=0, n_req=len(ok), host_lens=ok.ctypes.data, ws_bytes=16) == fk.ECAP
 
 
+def test_binding_host_lengths_are_one_int32_per_request():
+    """The binding hands the library a contiguous int32 copy of the host
+    lengths, one per request, or nothing."""
+    assert fk._host_lens(None, 3) is None
+    h = fk._host_lens([5, 0, 7], 3)
+    assert h.dtype == np.int32 and h.flags["C_CONTIGUOUS"] and h.tolist() == [5, 0, 7]
+    h64 = np.arange(8, dtype=np.int64)[::2]            # strided, int64
+    assert fk._host_lens(h64, 4).tolist() == [0, 2, 4, 6]
+    for bad in ([1, 2], [[1, 2, 3]], np.zeros((3, 1), np.int32)):
+        with pytest.raises(ValueError):
+            fk._host_lens(bad, 3)
+
+
 def attn_noalloc(p, layer=0, q=1 << 12, n_req=1, hq=8, hkv=2, dh=128, tables=1 << 16,
                  max_blocks=4, lens=1 << 18, max_seq=64, scale=0.1, split=0, out=1 << 20,
                  host_lens=None):
