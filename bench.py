@@ -177,7 +177,9 @@ def parse():
                     help="table3: comma-separated input lengths in tokens (default: Table 3's "
                          "500, 1000, 2000, 4000, 8000, 10000, 12000)")
     ap.add_argument("--steps", type=int, default=100, help="timed steps")
-    ap.add_argument("--warmup", type=int, default=10, help="untimed steps before them")
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed steps before them (default: 200 for attention, whose "
+                         "step needs about 25 ms of work to reach steady clocks, else 10)")
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="8b")
     ap.add_argument("--layout", choices=["block", "layer"], default="block",
                     help="pool layout of both sides: Eq. 5 block-major or per-layer")
@@ -217,7 +219,10 @@ def parse():
                     help="size of the plain copy run beside the kernel (HBM counter scale)")
     ap.add_argument("--calibration-only", action="store_true",
                     help="of the context rows run only the plain copy (for counter runs)")
-    return ap.parse_args()
+    args = ap.parse_args()
+    if args.warmup is None:
+        args.warmup = 200 if args.op == "attention" else 10
+    return args
 
 
 def kernel_hash(src: str = KERNEL_SRC) -> str:
@@ -313,12 +318,15 @@ def bench_attention(args):
         fk.flowkv_decode_attention(pool, layer, q, tab_d, lens_d, max_seq, scale, out, ws,
                                    args.split, seq_lens_host=host_lens if host else None)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    # the interpreter's garbage is collected before the warmup, not between
+    # it and the timed steps: after the GPU idles for a few tens of ms this
+    # step runs about 3% slower for the next ~25 ms of work
     evs = timing_pairs(args.steps)
     gc.collect()
     gc.disable()
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
     for e in evs:
         e[0].record()
@@ -1052,18 +1060,19 @@ def main():
     n_runs = len(segs)
     spot_check(receiver_list())
 
+    # Python's cyclic garbage collector is run before the warmup and kept off
+    # through the timed steps (as timeit does): a full collection of the
+    # interpreter's heap can stall the host for tens of milliseconds, and run
+    # between the warmup and the timed steps it would leave the GPU idle
+    # right before them
+    evs = timing_pairs(args.steps)
+    gc.collect()
+    gc.disable()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
     # ---- timed region -----------------------------------------------------------
-    evs = timing_pairs(args.steps)
-    # Python's cyclic garbage collector is run before and kept off during the
-    # timed steps (as timeit does): a full collection of the interpreter's
-    # heap can stall the host for tens of milliseconds mid-loop
-    gc.collect()
-    gc.disable()
-    torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         step(evs[i])
@@ -1174,12 +1183,12 @@ def main():
             segs_alt = step(fns=fns)
             torch.cuda.synchronize()
             spot_check(table_alt())
-            for _ in range(args.warmup):
-                step(fns=fns)
             evs_alt = timing_pairs(args.steps)
-            torch.cuda.synchronize()
             gc.collect()
             gc.disable()
+            for _ in range(args.warmup):
+                step(fns=fns)
+            torch.cuda.synchronize()
             t_alt = time.perf_counter()
             for e in evs_alt:
                 step(e, fns=fns)

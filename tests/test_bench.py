@@ -21,6 +21,18 @@ def test_bench_refuses_more_than_one_gpu():
     assert r.stdout == ""
 
 
+def test_bench_warmup_defaults_by_op(monkeypatch):
+    """Attention's default warmup covers the ~25 ms its step needs to reach
+    steady clocks after the GPU idled; an explicit --warmup is kept as given."""
+    import bench
+
+    for argv, want in ((["--op", "attention"], 200), ([], 10), (["--op", "table3"], 10),
+                       (["--op", "attention", "--warmup", "3"], 3),
+                       (["--warmup", "0"], 0)):
+        monkeypatch.setattr(sys, "argv", ["bench.py", *argv])
+        assert bench.parse().warmup == want, argv
+
+
 def run_bench(*args):
     import bench
 
