@@ -71,7 +71,7 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // Pass-1 workgroups: 8 waves on the vector units, 4 on the matrix cores.
 // (Eight waves per split, against four, took the 32-request batch from
-// 0.244 to 0.237 ms at its 1024-token splits, measured interleaved.)
+// 0.246 to 0.239 ms at its 1024-token splits, measured interleaved.)
 constexpr int kVecThreads = 512;
 constexpr int kMfmaThreads = 256;
 constexpr int kRowLanes = 16;              // lanes per token: one DPP row
