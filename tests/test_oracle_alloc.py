@@ -170,6 +170,24 @@ def test_shuffle_is_seeded_fisher_yates():
     assert shuffled_ids(1000, 123) == big and shuffled_ids(1000, 124) != big
 
 
+@pytest.mark.parametrize("P,seeds,chi2_limit", [(3, 6000, 20.5), (4, 24000, 49.7)])
+def test_shuffle_reaches_every_permutation_evenly(P, seeds, chi2_limit):
+    """Over consecutive seeds the shuffled free list takes each of the P!
+    orders about equally often (chi-square under its 0.1% critical value for
+    P! - 1 degrees of freedom).  Sattolo's variant (swap index drawn below i,
+    not up to i) reaches only the (P-1)! cyclic orders, and a skewed index
+    draw shifts the counts; both fail here."""
+    import collections
+    import itertools
+
+    perms = list(itertools.permutations(range(P)))
+    counts = collections.Counter(tuple(shuffled_ids(P, s)) for s in range(seeds))
+    assert set(counts) == set(perms)
+    expect = seeds / len(perms)
+    chi2 = sum((counts[p] - expect) ** 2 / expect for p in perms)
+    assert chi2 < chi2_limit, chi2
+
+
 def test_fifo_policies_order():
     a = RefAllocator(8, POLICY_FIFO_SORTED)
     a.mark_used([1, 4])
