@@ -121,3 +121,48 @@ def test_inline_transfer_replays_in_a_graph(sl, dl):
         assert torch.equal(blocks(dst, D), want), f"replay {i}: moved blocks differ"
         assert not blocks(dst, untouched).any(), f"replay {i}: wrote outside the plan"
     say("  3 replays move the plan's blocks and nothing else")
+
+
+@pytest.mark.parametrize("sl,dl", [(BM, BM), (LM, BM), (BM, LM)],
+                         ids=["block-block", "layer-block", "block-layer"])
+def test_per_layer_launches_replay_in_a_graph(sl, dl):
+    """The form the Table 3 sweep replays: one launch per layer with the plan
+    in device memory, all of them captured in one graph.  Each replay, after
+    the receiver was cleared, moves every layer of the plan's blocks and
+    nothing else."""
+    geom = Geometry("graph-layers", 6, 2, 64, 16, "bfloat16")
+    k = 37
+    B = 3 * k + 5
+    S = np.random.default_rng(31).permutation(B)[:2 * k].astype(np.int32)
+    D = (np.arange(2 * k, dtype=np.int32) // 2) * 3 + (np.arange(2 * k) % 2)
+    segs = fk.flowkv_plan(S, D.astype(np.int32), B, B)
+    n = len(S)
+    src = fk.KVPool(sl, make_device_pool(geom, sl, B, "cuda", 41))
+    dst = fk.KVPool(dl, make_device_pool(geom, dl, B, "cuda", 42))
+    segs_dev = fk.segments_to_device(segs, src.device)
+    torch.cuda.synchronize()
+    say(f"graph capture: {geom.num_layers} per-layer launches, {len(segs)} runs")
+
+    def blocks(pool, ids):   # (len(ids), L, 2, chunk) bytes in either layout
+        idx = torch.as_tensor(np.asarray(ids, dtype=np.int64), device="cuda")
+        if pool.layout == BM:
+            return pool.tensors[0].index_select(0, idx).view(torch.uint8).reshape(
+                len(ids), geom.num_layers, 2, -1)
+        per = [t.index_select(1, idx).view(torch.uint8).reshape(2, len(ids), -1)
+               for t in pool.tensors]
+        return torch.stack(per, 0).permute(2, 0, 1, 3)
+
+    want = blocks(src, S).clone()
+    untouched = np.setdiff1d(np.arange(B), D)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for layer in range(geom.num_layers):
+            fk.flowkv_transfer_layers(src, dst, segs_dev, len(segs), n, layer, 1)
+    for i in range(3):
+        for t in dst.tensors:                   # eager work between replays
+            t.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(blocks(dst, D), want), f"replay {i}: moved blocks differ"
+        assert not blocks(dst, untouched).any(), f"replay {i}: wrote outside the plan"
+    say("  3 replays move every layer of the plan's blocks and nothing else")
