@@ -275,12 +275,12 @@ def fit_receiver_blocks(free_bytes: int, src_blocks: int, dst_blocks: int,
     return max(0, room // block_bytes // 4096 * 4096)
 
 
-def bench_attention(args):
+def attention_setup(attn_workload: str, layout_name: str, split: int):
     """Decode attention (one layer, one new token per request) over the
-    receiver pool and block lists of a transfer workload: by default the
-    32-request batch (32 query heads on 8 KV heads, head_dim 128, block 16,
-    2,000-20,000 tokens per request); also the 13,000-token request and one
-    GPU's share of Llama-3-70B at TP=8 (8 query heads on 1 KV head)."""
+    receiver pool and block lists of a transfer workload: the step, with the
+    lengths carried on the host when they fit, and its algorithmic bytes."""
+    import types
+
     import numpy as np
     import torch
 
@@ -289,8 +289,8 @@ def bench_attention(args):
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    layout = fk.LAYOUT_BLOCK_MAJOR if args.layout == "block" else fk.LAYOUT_LAYER_MAJOR
-    recipe, rargs, q_heads, label = ATTN_WORKLOADS[args.attn_workload]
+    layout = fk.LAYOUT_BLOCK_MAJOR if layout_name == "block" else fk.LAYOUT_LAYER_MAJOR
+    recipe, rargs, q_heads, label = ATTN_WORKLOADS[attn_workload]
     wl = getattr(recipes, recipe)(lambda P, pol, seed: fk.Allocator(P, pol, seed), *rargs)
     geom = wl.geom
     pool = fk.KVPool(layout, make_device_pool(geom, layout, wl.dst_pool_blocks, dev, seed=1))
@@ -305,7 +305,7 @@ def bench_attention(args):
     out = torch.empty((len(lens), q_heads, geom.head_dim), dtype=torch.float32, device=dev)
     max_seq = int(lens.max())
     ws = torch.empty(fk.flowkv_decode_attention_workspace(len(lens), q_heads, geom.head_dim,
-                                                          max_seq, args.split),
+                                                          max_seq, split),
                      dtype=torch.uint8, device=dev)
     scale = 1.0 / geom.head_dim ** 0.5
     layer = geom.num_layers // 2
@@ -316,26 +316,89 @@ def bench_attention(args):
 
     def step(host=True):
         fk.flowkv_decode_attention(pool, layer, q, tab_d, lens_d, max_seq, scale, out, ws,
-                                   args.split, seq_lens_host=host_lens if host else None)
+                                   split, seq_lens_host=host_lens if host else None)
+
+    split_used = split or fk.flowkv_decode_attention_split(len(lens), max_seq)
+    kv_bytes = int(lens.sum()) * 2 * geom.kv_heads * geom.head_dim * 2
+    # workspace: written by pass 1 and read by pass 2, for the splits that exist
+    used_splits = int(sum(-(-int(T) // split_used) for T in lens))
+    ws_bytes = 2 * used_splits * q_heads * (geom.head_dim + 2) * 4
+    algo = kv_bytes + q.numel() * 2 + out.numel() * 4 + ws_bytes + tab.nbytes
+    return types.SimpleNamespace(step=step, algo=algo, label=label, split=split_used,
+                                 pool=pool, geom=geom, layer=layer, q=q, wl=wl, lens=lens,
+                                 scale=scale, q_heads=q_heads, host_lens=host_lens,
+                                 layout=layout_name, dev=dev)
+
+
+def attention_time(step, steps: int, warmup: int):
+    """Mean kernel time (ms, HIP events around each step) and wall time (s)
+    of `steps` back-to-back steps after `warmup` untimed ones."""
+    import torch
 
     # the interpreter's garbage is collected before the warmup, not between
     # it and the timed steps: after the GPU idles for a few tens of ms this
     # step runs about 3% slower for the next ~25 ms of work
-    evs = timing_pairs(args.steps)
+    evs = timing_pairs(steps)
     gc.collect()
     gc.disable()
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for e in evs:
-        e[0].record()
-        step()
-        e[1].record()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    gc.enable()
-    ms = statistics.fmean(a.elapsed_time(b) for a, b in evs)
+    try:
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for e in evs:
+            e[0].record()
+            step()
+            e[1].record()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+    finally:
+        gc.enable()
+    ts = [a.elapsed_time(b) for a, b in evs]
+    return statistics.fmean(ts), elapsed, ts
+
+
+def attention_context(steps: int) -> dict:
+    """The attention bench's default step (the 32-request batch over a
+    block-major pool), timed the same way, for the transfer bench's line."""
+    try:
+        a = attention_setup("batch", "block", 0)
+        ms, elapsed, ts = attention_time(a.step, steps, 200)
+        import numpy as np
+        row = {"workload": a.label, "split_tokens": a.split, "steps": steps, "warmup": 200,
+               "kernel_ms_avg": round(ms, 4),
+               "kernel_ms_p10_p50_p90": [round(float(x), 4)
+                                         for x in np.percentile(ts, [10, 50, 90])],
+               "hbm_gbps": round(a.algo / (ms * 1e-3) / 1e9, 1),
+               "roofline_frac": round(a.algo / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+               "note": "bench.py --op attention's step in the same run (decode_attn_split + "
+                       "decode_attn_merge), after the transfer pools were freed"}
+        del a
+        return row
+    except Exception as e:  # reported in the line, never a reason to lose it
+        row = {"error": f"{type(e).__name__}: {e}"[:300]}
+        try:
+            import torch
+            row["allocated_gib"] = round(torch.cuda.memory_allocated() / 2**30, 2)
+        except Exception:
+            pass
+        return row
+
+
+def bench_attention(args):
+    """Decode attention (one layer, one new token per request) over the
+    receiver pool and block lists of a transfer workload: by default the
+    32-request batch (32 query heads on 8 KV heads, head_dim 128, block 16,
+    2,000-20,000 tokens per request); also the 13,000-token request and one
+    GPU's share of Llama-3-70B at TP=8 (8 query heads on 1 KV head)."""
+    import numpy as np
+    import torch
+
+    a = attention_setup(args.attn_workload, args.layout, args.split)
+    step, algo, split, host_lens = a.step, a.algo, a.split, a.host_lens
+    pool, geom, layer, q, wl, lens, scale = a.pool, a.geom, a.layer, a.q, a.wl, a.lens, a.scale
+    q_heads, label, dev = a.q_heads, a.label, a.dev
+    ms, elapsed, ts = attention_time(step, args.steps, args.warmup)
 
     context = {}
     ab = None
@@ -379,12 +442,6 @@ def bench_attention(args):
     if not args.no_cpu_baseline:
         cpu = attention_cpu_baseline(pool, geom, layer, q, wl, lens, scale, np, torch)
 
-    kv_bytes = int(lens.sum()) * 2 * geom.kv_heads * geom.head_dim * 2
-    split = args.split or fk.flowkv_decode_attention_split(len(lens), max_seq)
-    # workspace: written by pass 1 and read by pass 2, for the splits that exist
-    used_splits = int(sum(-(-int(T) // split) for T in lens))
-    ws_bytes = 2 * used_splits * q_heads * (geom.head_dim + 2) * 4
-    algo = kv_bytes + q.numel() * 2 + out.numel() * 4 + ws_bytes + tab.nbytes
     achieved = algo / (ms * 1e-3) / 1e9
     if ab is not None:
         context["lengths_in_arguments_vs_device"] = {
@@ -406,8 +463,7 @@ def bench_attention(args):
                    "lengths_in": ("kernel-arguments" if host_lens is not None
                                   else "device-memory")},
         "kernel_ms_avg": round(ms, 4),
-        "kernel_ms_p10_p50_p90": [round(float(x), 4) for x in
-                                  np.percentile([a.elapsed_time(b) for a, b in evs], [10, 50, 90])],
+        "kernel_ms_p10_p50_p90": [round(float(x), 4) for x in np.percentile(ts, [10, 50, 90])],
         "timing_events": TIMING["events"],
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
@@ -1347,6 +1403,16 @@ def main():
         "context": context,
         "setup_s": round(setup_s, 2),
     }
+    # the decode attention that reads the receiver pool, timed in the same
+    # run (the default line only): the transfer pools are freed first
+    if (single and not args.no_context and not args.calibration_only and not args.layerwise
+            and args.workload == "8b" and args.layout == "block"):
+        # (the comparators above left views of the pools in these names)
+        sv = dv = ts = td = None  # noqa: F841
+        del src, dst, stager
+        gc.collect()
+        torch.cuda.empty_cache()
+        context["decode_attention"] = attention_context(args.steps)
     print(json.dumps(line), flush=True)
 
 

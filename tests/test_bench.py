@@ -33,6 +33,19 @@ def test_bench_warmup_defaults_by_op(monkeypatch):
         assert bench.parse().warmup == want, argv
 
 
+def test_attention_row_reports_a_failure_instead_of_raising():
+    """The transfer line's decode-attention row never costs the line: where
+    the attention step cannot run (here: no GPU) the row holds the error."""
+    import torch
+
+    import bench
+
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present: the row would run")
+    row = bench.attention_context(3)
+    assert set(row) <= {"error", "allocated_gib"} and row["error"]
+
+
 def run_bench(*args):
     import bench
 
