@@ -206,6 +206,23 @@ def test_host_lengths_give_identical_outputs(layout, shape):
     say(f"  identical to the device-lengths call; max error {err:.2e}")
 
 
+@pytest.mark.parametrize("n_req", [fk.ATTN_INLINE_LENS, fk.ATTN_INLINE_LENS + 1])
+def test_host_lengths_at_the_argument_capacity(n_req):
+    """At most ATTN_INLINE_LENS host lengths ride in the kernel arguments;
+    one request more and the call reads the lengths on the device instead.
+    Either way the outputs equal the device-lengths call bit for bit and
+    pass the oracle."""
+    geom = Geometry("cap", 2, 2, 64, 16, "bfloat16")
+    g = np.random.default_rng(n_req)
+    lens = [int(x) for x in g.integers(1, 48, size=n_req)]
+    blocks = sum(-(-T // 16) for T in lens) + 4
+    say(f"host lengths at capacity: {n_req} requests, {sum(lens)} tokens")
+    dev_out, _ = run_case(geom, BM, blocks, lens, 4, 90, check=False)
+    host_out, err = run_case(geom, BM, blocks, lens, 4, 90, host_lens=True)
+    assert np.array_equal(dev_out, host_out)
+    say(f"  identical to the device-lengths call; max error {err:.2e}")
+
+
 def test_length_caps_and_empty_request():
     """Tokens past max_seq_len are not read; a zero-length request gives zeros."""
     geom = Geometry("caps", 2, 2, 64, 16, "bfloat16")
