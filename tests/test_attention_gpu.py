@@ -223,6 +223,36 @@ def test_host_lengths_at_the_argument_capacity(n_req):
     say(f"  identical to the device-lengths call; max error {err:.2e}")
 
 
+@pytest.mark.parametrize("hq,hkv,dh", [(8, 1, 128), (4, 2, 64)],
+                         ids=["matrix-core-pass", "vector-pass"])
+def test_most_requests_one_token_each(hq, hkv, dh):
+    """65,535 requests (the grid's limit) of one token each: a softmax over
+    one token weighs it exactly 1, so every output is that token's V, bit
+    for bit (bf16 values are exact in float32), gathered here with torch's
+    own indexing."""
+    n = 65535
+    geom = Geometry("many", 1, hkv, dh, 16, "bfloat16")
+    B = n + 3
+    g = np.random.default_rng(5)
+    blk = g.permutation(B)[:n].astype(np.int32)
+    pool = fk.KVPool(BM, make_device_pool(geom, BM, B, "cuda", 5))
+    tab = torch.as_tensor(blk.reshape(n, 1), device="cuda")
+    lens = torch.ones(n, dtype=torch.int32, device="cuda")
+    q = torch.randn((n, hq, dh), generator=torch.Generator("cuda").manual_seed(6),
+                    device="cuda").to(torch.bfloat16)
+    ws = torch.empty(fk.flowkv_decode_attention_workspace(n, hq, dh, 1), dtype=torch.uint8,
+                     device="cuda")
+    out = torch.full((n, hq, dh), float("nan"), dtype=torch.float32, device="cuda")
+    say(f"{n} one-token requests, {hq} query heads on {hkv}, head_dim {dh}")
+    fk.flowkv_decode_attention(pool, 0, q, tab, lens, 1, 0.1, out, ws)
+    torch.cuda.synchronize()
+    # block-major pool: (B, L, 2, bs, Hkv, Dh); V of layer 0, slot 0
+    v = pool.tensors[0].view(B, 1, 2, 16, hkv, dh)[torch.as_tensor(blk.astype(np.int64),
+                                                                   device="cuda"), 0, 1, 0]
+    want = v.float().repeat_interleave(hq // hkv, dim=1)   # query head h reads KV head h // G
+    assert torch.equal(out, want)
+
+
 def test_length_caps_and_empty_request():
     """Tokens past max_seq_len are not read; a zero-length request gives zeros."""
     geom = Geometry("caps", 2, 2, 64, 16, "bfloat16")
