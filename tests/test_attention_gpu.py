@@ -253,6 +253,37 @@ def test_most_requests_one_token_each(hq, hkv, dh):
     assert torch.equal(out, want)
 
 
+@pytest.mark.parametrize("host_lens", [False, True], ids=["lengths-on-device", "lengths-on-host"])
+@pytest.mark.parametrize("hq,hkv,dh", [(8, 1, 128), (4, 2, 64)],
+                         ids=["matrix-core-pass", "vector-pass"])
+def test_most_splits_constant_values(hq, hkv, dh, host_lens):
+    """One 65,535-token request in one-token splits: 65,535 pass-1 workgroups
+    per KV head (the grid's limit) and as many records for the merge.  With a
+    zero query every weight is exactly 1, and with V constant per KV head
+    every partial sum is an exact multiple of that constant, so each output
+    is the constant, bit for bit."""
+    T = 65535
+    geom = Geometry("splits", 1, hkv, dh, 16, "bfloat16")
+    B = -(-T // 16) + 2
+    pool = fk.KVPool(BM, make_device_pool(geom, BM, B, "cuda", 8))
+    consts = torch.tensor([0.75, -3.0][:hkv], dtype=torch.bfloat16, device="cuda")
+    kv = pool.tensors[0].view(B, 1, 2, 16, hkv, dh)
+    kv[:, 0, 1] = consts.view(1, 1, hkv, 1)          # V of every slot: its head's constant
+    blk = np.random.default_rng(8).permutation(B)[:-(-T // 16)].astype(np.int32)
+    tab = torch.as_tensor(blk.reshape(1, -1), device="cuda")
+    lens = torch.tensor([T], dtype=torch.int32, device="cuda")
+    q = torch.zeros((1, hq, dh), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(fk.flowkv_decode_attention_workspace(1, hq, dh, T, 1), dtype=torch.uint8,
+                     device="cuda")
+    out = torch.full((1, hq, dh), float("nan"), dtype=torch.float32, device="cuda")
+    say(f"one {T}-token request in {T} splits, {hq} query heads on {hkv}, head_dim {dh}")
+    fk.flowkv_decode_attention(pool, 0, q, tab, lens, T, 0.1, out, ws, 1,
+                               seq_lens_host=np.array([T], np.int32) if host_lens else None)
+    torch.cuda.synchronize()
+    want = consts.float().repeat_interleave(hq // hkv).view(1, hq, 1).expand(1, hq, dh)
+    assert torch.equal(out, want)
+
+
 def test_length_caps_and_empty_request():
     """Tokens past max_seq_len are not read; a zero-length request gives zeros."""
     geom = Geometry("caps", 2, 2, 64, 16, "bfloat16")
