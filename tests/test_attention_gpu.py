@@ -284,6 +284,17 @@ def test_most_splits_constant_values(hq, hkv, dh, host_lens):
     assert torch.equal(out, want)
 
 
+@pytest.mark.parametrize("layout", [BM, LM], ids=lambda x: NAMES[x])
+@pytest.mark.parametrize("layer", [0, fk.MAX_LAYERS - 1], ids=["first-layer", "last-layer"])
+def test_deepest_pool_first_and_last_layer(layout, layer):
+    """Pools of the most layers the library takes: the last layer's base
+    pointer (layer-major) or its offset inside a block (block-major) against
+    the oracle."""
+    geom = Geometry("deep", fk.MAX_LAYERS, 2, 64, 16, "bfloat16")
+    say(f"{fk.MAX_LAYERS}-layer {NAMES[layout]} pool, layer {layer}")
+    run_case(geom, layout, 24, [37, 150, 1], 4, 11, layer=layer)
+
+
 def test_length_caps_and_empty_request():
     """Tokens past max_seq_len are not read; a zero-length request gives zeros."""
     geom = Geometry("caps", 2, 2, 64, 16, "bfloat16")
