@@ -379,6 +379,31 @@ def test_layer_ranges_against_oracle(seed):
     assert host_equal(download_all(dst), h_dst)
 
 
+@pytest.mark.parametrize("l0,lc", [(127, 1), (0, 128), (64, 64)],
+                         ids=["last-layer", "all-layers", "upper-half"])
+def test_layer_ranges_of_the_deepest_pools(l0, lc):
+    """Layer ranges at the top of 128-layer pools, in all four layout pairs,
+    on both address paths (H = 3,840 B: per-lane; H = 4 KiB at 256 threads:
+    uniform), against the oracle over the whole receiver pool."""
+    tables = [(np.array([8, 0, 7, 1], np.int32), np.array([6, 5, 0, 1], np.int32))]
+    for geom, cfg in ((Geometry("deep-lane", 128, 3, 40, 16, "bfloat16"), {}),
+                      (Geometry("deep-uni", 128, 1, 128, 16, "bfloat16"), dict(threads=256))):
+        for sl, dl in LAYOUT_PAIRS:
+            say(f"layers [{l0}, {l0 + lc}) of 128, H={geom.chunk_bytes} {NAMES[sl]}->{NAMES[dl]}")
+            src = device_pool(geom, sl, 9, 3)
+            dst = device_pool(geom, dl, 7, 4)
+            h_src, h_dst = download_all(src), download_all(dst)
+            segs, S, D = plan_tables(tables, 9, 7)
+            dev = fk.segments_to_device(segs, src.device)
+            fk.flowkv_transfer_layers(src, dst, dev, len(segs), fk.plan_total_blocks(segs), l0,
+                                      lc, **cfg)
+            torch.cuda.synchronize()
+            for s_, d_ in tables:
+                oracle.transfer_fast(h_src, h_dst, s_, d_, layers=range(l0, l0 + lc))
+            got = download_all(dst)
+            assert host_equal(got, h_dst), first_mismatch(got, h_dst)
+
+
 @pytest.mark.parametrize("sl,dl", [(BM, BM), (LM, LM)], ids=lambda x: NAMES[x])
 def test_one_launch_per_layer_equals_one_launch(sl, dl):
     """The 8B geometry (32 layers): 32 per-layer launches give the same
