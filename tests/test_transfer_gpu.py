@@ -404,6 +404,36 @@ def test_layer_ranges_of_the_deepest_pools(l0, lc):
             assert host_equal(got, h_dst), first_mismatch(got, h_dst)
 
 
+@pytest.mark.parametrize("sl,dl", [(BM, BM), (LM, BM)], ids=lambda x: NAMES[x])
+def test_concurrent_requests_on_separate_streams(sl, dl):
+    """The copy keeps no state between launches: four requests moved at once
+    on four streams (plans in the kernel arguments, disjoint receiver blocks)
+    leave the receiver exactly as the oracle moving them one after another."""
+    geom = Geometry("streams", 4, 2, 64, 16, "bfloat16")
+    B = 160
+    g = np.random.default_rng(77)
+    src_ids = g.permutation(B).astype(np.int32)
+    dst_ids = g.permutation(B).astype(np.int32)
+    sizes = [40, 1, 23, 60]
+    tables, pos = [], 0
+    for k in sizes:
+        tables.append((src_ids[pos:pos + k], dst_ids[pos:pos + k]))
+        pos += k
+    src = device_pool(geom, sl, B, 5)
+    dst = device_pool(geom, dl, B, 6)
+    h_src, h_dst = download_all(src), download_all(dst)
+    streams = [torch.cuda.Stream() for _ in tables]    # default priority
+    torch.cuda.synchronize()
+    for (s_, d_), st in zip(tables, streams):
+        segs = fk.flowkv_plan(s_, d_, B, B)
+        fk.flowkv_transfer_inline(src, dst, segs, len(s_), stream=st)
+    torch.cuda.synchronize()
+    for s_, d_ in tables:
+        oracle.transfer_fast(h_src, h_dst, s_, d_)
+    got = download_all(dst)
+    assert host_equal(got, h_dst), first_mismatch(got, h_dst)
+
+
 @pytest.mark.parametrize("sl,dl", [(BM, BM), (LM, LM)], ids=lambda x: NAMES[x])
 def test_one_launch_per_layer_equals_one_launch(sl, dl):
     """The 8B geometry (32 layers): 32 per-layer launches give the same
