@@ -36,8 +36,9 @@ Parity: the policy itself is underspecified in the paper, so agreement with
 the paper's allocator is "parity unpinned".  The reading above is pinned in
 ``tests/test_oracle_alloc.py`` by exhaustive minimal-segment optimality over
 every free bitmap of small pools, best-fit and head placement checked against
-brute-force enumeration, conservation and no-double-assignment invariants, and
-the published SplitMix64 output for seed 0.
+brute-force enumeration, conservation and no-double-assignment invariants,
+the published SplitMix64 output for seed 0, and the shuffle reaching every
+order of 3 and 4 blocks about equally often over consecutive seeds.
 """
 
 from __future__ import annotations
