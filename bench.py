@@ -1199,12 +1199,14 @@ def main():
                     for r in range(2 * geom.num_layers):
                         dv[int(D[i]), r].copy_(sv[int(S_all[i]), r])
                         calls += 1
+                del sv, dv
             else:
                 for ts, td in zip(src.tensors, dst.tensors):
                     for kv in range(2):
                         for i in range(n):
                             td[kv, int(D[i])].copy_(ts[kv, int(S_all[i])])
                             calls += 1
+                del ts, td
             torch.cuda.synchronize()
             context["per_chunk_copy_calls"] = calls
             context["per_chunk_copy_ms"] = round((time.perf_counter() - t_chunks) * 1e3, 2)
@@ -1227,6 +1229,7 @@ def main():
                             m = int(sg["n_blocks"])
                             td[kv, d0:d0 + m].copy_(ts[kv, s0:s0 + m])
                             calls += 1
+                del ts, td
             torch.cuda.synchronize()
             context["per_run_copy_calls"] = calls
             context["per_run_copy_ms"] = round((time.perf_counter() - t_runs) * 1e3, 3)
@@ -1407,8 +1410,6 @@ def main():
     # run (the default line only): the transfer pools are freed first
     if (single and not args.no_context and not args.calibration_only and not args.layerwise
             and args.workload == "8b" and args.layout == "block"):
-        # (the comparators above left views of the pools in these names)
-        sv = dv = ts = td = None  # noqa: F841
         del src, dst, stager
         gc.collect()
         torch.cuda.empty_cache()
