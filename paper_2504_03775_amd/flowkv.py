@@ -578,6 +578,10 @@ def _check_attention_tensors(pool: KVPool, q, block_tables, seq_lens, out):
     import torch
 
     n, hq, dh = q.shape
+    # the kernels read K and V as bfloat16; the C ABI sees only byte sizes,
+    # so a pool of another 2-byte type is refused here
+    if any(t.dtype != torch.bfloat16 for t in pool.tensors):
+        raise ValueError(f"attention reads bfloat16 K/V: the pool holds {pool.tensors[0].dtype}")
     for t, dt in ((q, torch.bfloat16), (block_tables, torch.int32), (seq_lens, torch.int32),
                   (out, torch.float32)):
         if t.dtype != dt or not t.is_contiguous() or t.device != pool.device:

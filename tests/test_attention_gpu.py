@@ -295,6 +295,23 @@ def test_deepest_pool_first_and_last_layer(layout, layer):
     run_case(geom, layout, 24, [37, 150, 1], 4, 11, layer=layer)
 
 
+def test_pool_of_another_type_is_refused():
+    """The kernels read bf16 K/V; an fp16 pool of the same byte size (the
+    transfer moves either) is refused by the binding, not misread."""
+    geom = Geometry("fp16", 2, 2, 64, 16, "float16")
+    pool = fk.KVPool(BM, make_device_pool(geom, BM, 8, "cuda", 1))
+    q = torch.zeros((1, 4, 64), dtype=torch.bfloat16, device="cuda")
+    tab = torch.zeros((1, 1), dtype=torch.int32, device="cuda")
+    lens = torch.ones(1, dtype=torch.int32, device="cuda")
+    out = torch.empty((1, 4, 64), dtype=torch.float32, device="cuda")
+    ws = torch.empty(fk.flowkv_decode_attention_workspace(1, 4, 64, 1), dtype=torch.uint8,
+                     device="cuda")
+    with pytest.raises(ValueError, match="bfloat16"):
+        fk.flowkv_decode_attention(pool, 0, q, tab, lens, 1, 0.1, out, ws)
+    with pytest.raises(ValueError, match="bfloat16"):
+        fk.flowkv_decode_attention_noalloc(pool, 0, q, tab, lens, 1, 0.1, out)
+
+
 def test_length_caps_and_empty_request():
     """Tokens past max_seq_len are not read; a zero-length request gives zeros."""
     geom = Geometry("caps", 2, 2, 64, 16, "bfloat16")
