@@ -466,11 +466,21 @@ def _stream_handle(stream) -> Optional[int]:
     return stream.cuda_stream
 
 
+def _pools(src: KVPool, dst: KVPool):
+    """The two descriptors, by reference, for a copy between pools of one
+    element type: the library compares byte geometry only, so bf16 into fp16
+    (same sizes, other encoding) is refused here."""
+    if src.tensors[0].dtype != dst.tensors[0].dtype:
+        raise ValueError(f"pools of different element types: {src.tensors[0].dtype} and "
+                         f"{dst.tensors[0].dtype}")
+    return ctypes.byref(src.desc), ctypes.byref(dst.desc)
+
+
 def flowkv_transfer(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_blocks: int,
                     stream=None) -> None:
     """Enqueue the one-launch copy; segs_dev is a device int32 (k, 4) tensor
     on the pools' device."""
-    _check(_lib.flowkv_transfer(ctypes.byref(src.desc), ctypes.byref(dst.desc),
+    _check(_lib.flowkv_transfer(*_pools(src, dst),
                                 ctypes.c_void_p(_device_segments(segs_dev, n_segs, src)),
                                 n_segs, total_blocks, ctypes.c_void_p(_stream_handle(stream))),
            "flowkv_transfer")
@@ -480,7 +490,7 @@ def flowkv_transfer_ex(src: KVPool, dst: KVPool, segs_dev, n_segs: int, total_bl
                        threads: int = 0, unroll: int = 0, grid: int = 0, cache: int = 0,
                        order: int = 0, stream=None) -> None:
     cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
-    _check(_lib.flowkv_transfer_ex(ctypes.byref(src.desc), ctypes.byref(dst.desc),
+    _check(_lib.flowkv_transfer_ex(*_pools(src, dst),
                                    ctypes.c_void_p(_device_segments(segs_dev, n_segs, src)),
                                    n_segs, total_blocks, ctypes.byref(cfg),
                                    ctypes.c_void_p(_stream_handle(stream))),
@@ -506,7 +516,7 @@ def flowkv_transfer_inline(src: KVPool, dst: KVPool, segs: np.ndarray, total_blo
     and neither has more than INLINE_LAYERS layers (``inline_capacity``)."""
     segs = _host_segments(segs)
     cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
-    _check(_lib.flowkv_transfer_inline(ctypes.byref(src.desc), ctypes.byref(dst.desc),
+    _check(_lib.flowkv_transfer_inline(*_pools(src, dst),
                                        _ptr(segs), len(segs), total_blocks,
                                        ctypes.byref(cfg), ctypes.c_void_p(_stream_handle(stream))),
            "flowkv_transfer_inline")
@@ -523,7 +533,7 @@ def flowkv_transfer_request(src: KVPool, dst: KVPool, src_ids, dst_ids, threads:
         raise ValueError("sender and receiver lists differ in length")
     cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
     n = ctypes.c_int64()
-    _check(_lib.flowkv_transfer_request(ctypes.byref(src.desc), ctypes.byref(dst.desc),
+    _check(_lib.flowkv_transfer_request(*_pools(src, dst),
                                         _ptr(s), _ptr(d), s.size, ctypes.byref(cfg),
                                         ctypes.byref(n), ctypes.c_void_p(_stream_handle(stream))),
            "flowkv_transfer_request")
@@ -535,7 +545,7 @@ def flowkv_transfer_layers(src: KVPool, dst: KVPool, segs_dev, n_segs: int, tota
                            grid: int = 0, cache: int = 0, order: int = 0, stream=None) -> None:
     """Enqueue the copy of layers [layer_begin, layer_begin + layer_count) only."""
     cfg = flowkv_launch_config(threads, unroll, grid, cache, order)
-    _check(_lib.flowkv_transfer_layers(ctypes.byref(src.desc), ctypes.byref(dst.desc),
+    _check(_lib.flowkv_transfer_layers(*_pools(src, dst),
                                        ctypes.c_void_p(_device_segments(segs_dev, n_segs, src)),
                                        n_segs, total_blocks, layer_begin, layer_count,
                                        ctypes.byref(cfg), ctypes.c_void_p(_stream_handle(stream))),

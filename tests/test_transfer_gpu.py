@@ -404,6 +404,24 @@ def test_layer_ranges_of_the_deepest_pools(l0, lc):
             assert host_equal(got, h_dst), first_mismatch(got, h_dst)
 
 
+def test_pools_of_different_element_types_are_refused():
+    """bf16 into fp16 has the same byte geometry, which is all the library
+    compares; the binding refuses the pair before any launch."""
+    a = device_pool(Geometry("bf", 2, 2, 64, 16, "bfloat16"), BM, 8, 0)
+    b = device_pool(Geometry("fp", 2, 2, 64, 16, "float16"), BM, 8, 1)
+    before = b.tensors[0].clone()
+    segs = fk.flowkv_plan([0, 1], [2, 3], 8, 8)
+    dev = fk.segments_to_device(segs, a.device)
+    for call in (lambda: fk.flowkv_transfer_inline(a, b, segs, 2),
+                 lambda: fk.flowkv_transfer(a, b, dev, len(segs), 2),
+                 lambda: fk.flowkv_transfer_layers(b, a, dev, len(segs), 2, 0, 1),
+                 lambda: fk.flowkv_transfer_request(a, b, [0, 1], [2, 3])):
+        with pytest.raises(ValueError, match="element types"):
+            call()
+    torch.cuda.synchronize()
+    assert torch.equal(b.tensors[0], before)
+
+
 @pytest.mark.parametrize("sl,dl", [(BM, BM), (LM, BM)], ids=lambda x: NAMES[x])
 def test_concurrent_requests_on_separate_streams(sl, dl):
     """The copy keeps no state between launches: four requests moved at once
