@@ -166,3 +166,49 @@ def test_per_layer_launches_replay_in_a_graph(sl, dl):
         assert torch.equal(blocks(dst, D), want), f"replay {i}: moved blocks differ"
         assert not blocks(dst, untouched).any(), f"replay {i}: wrote outside the plan"
     say("  3 replays move every layer of the plan's blocks and nothing else")
+
+
+def test_request_and_workspace_attention_replay_in_a_graph():
+    """Two more entry points that allocate nothing during the call: the
+    one-call request transfer (its plan is built on the host stack and
+    rides in the kernel arguments) and attention with the caller's
+    workspace.  Captured together, replayed after the receiver and the
+    output were cleared, each replay reproduces the eager results."""
+    geom = Geometry("graph-both", 3, 2, 128, 16, "bfloat16")
+    B = 96
+    g = np.random.default_rng(51)
+    S = g.permutation(B)[:40].astype(np.int32)
+    D = g.permutation(B)[:40].astype(np.int32)
+    src = fk.KVPool(BM, make_device_pool(geom, BM, B, "cuda", 52))
+    dst = fk.KVPool(BM, make_device_pool(geom, BM, B, "cuda", 53))
+    lens = np.array([600, 17], np.int32)
+    tab = torch.as_tensor(np.stack([D[:38], np.r_[D[38:], -np.ones(36, np.int32)]]),
+                          device="cuda")
+    lens_d = torch.as_tensor(lens, device="cuda")
+    q = torch.randn((2, 8, 128), generator=torch.Generator("cuda").manual_seed(54),
+                    device="cuda").to(torch.bfloat16)
+    ws = torch.empty(fk.flowkv_decode_attention_workspace(2, 8, 128, 600), dtype=torch.uint8,
+                     device="cuda")
+    say("graph capture: request transfer, then attention over the moved blocks")
+
+    def both(out):
+        fk.flowkv_transfer_request(src, dst, S, D)
+        fk.flowkv_decode_attention(dst, 1, q, tab, lens_d, 600, 0.088, out, ws)
+
+    pre = dst.tensors[0].clone()
+    eager = torch.empty((2, 8, 128), dtype=torch.float32, device="cuda")
+    both(eager)
+    torch.cuda.synchronize()
+    moved = dst.tensors[0].clone()
+    out = torch.empty_like(eager)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        both(out)
+    for i in range(3):
+        dst.tensors[0].copy_(pre)               # eager work between replays
+        out.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(dst.tensors[0], moved), f"replay {i}: receiver differs"
+        assert torch.equal(out, eager), f"replay {i}: attention differs"
+    say("  3 replays equal the eager calls")
