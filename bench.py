@@ -637,8 +637,7 @@ hipMemcpyDeviceToDeviceNoCU, one call per run, layer and K-or-V):
     out, so the stand-in is shorter than a real prefill.  `value` is the
     transfer time the layer-wise overlap leaves exposed after the prefill:
     the median over rounds of (overlapped step - prefill-alone step), the
-    four forms running interleaved, once per round.""" 
-    import numpy as np
+    four forms running interleaved, once per round."""
     import torch
 
     from paper_2504_03775_amd import flowkv as fk
@@ -822,7 +821,6 @@ def bench_table3(args):
     latency (plan, staging, launches and kernels, synchronised; median of
     20).  `value` is the mean synchronised one-launch latency over the
     lengths (the paper's column mean, 0.0309 s on one L20 server)."""
-    import numpy as np
     import torch
 
     from paper_2504_03775_amd import flowkv as fk
